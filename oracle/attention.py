@@ -1,0 +1,126 @@
+"""Plain, unfused float64 attention — the oracle (test infrastructure only).
+
+Follows, step by step and in the same order, the paper's compute definition
+of attention (appendix figure "Compute definition for the attention operator")
+and Eq. attention of the appendix "Additional Example Operators":
+
+    p      = q . k^T                                 (batch_matmul, trans_b)
+    score  = mask ? score_mod(p) : -inf              (if_then_else)
+    m_i    = max_j score_ij                          (softmax_maxelem)
+    e_ij   = exp(score_ij - m_i)                     (softmax_exp)
+    s_i    = sum_j e_ij                              (softmax_expsum)
+    o_id   = sum_j e_ij v_jd                         (second batch_matmul)
+    o'_id  = o_id / s_i                              (softmax_norm)
+
+Everything is float64; the fp16/bf16 inputs are upcast exactly by the caller.
+The score matrix S and the matrix E (and P = E / s) are materialised in full
+for each (batch, query head): nothing is blocked, fused or reordered.
+
+Readings taken where the paper is silent or garbled (each one is listed in the
+design notes):
+
+* Eq. attention prints the first product as q . v; the compute definition
+  multiplies q by k transposed, which is what is used here.
+* ``score_mod(p) = p * scale + bias``: the scale multiplies q.k only and the
+  bias is added after scaling.  ``scale`` is an argument (1/sqrt(D) in every
+  workload).
+* Masked entries are -inf whatever the bias is.
+* Causal masking is aligned bottom-right: query row i sees key j iff
+  j <= i + (Lk - Lq).  With Lq == Lk this is j <= i; with Lq == 1 (decode)
+  every key is visible.
+* A row that sees no key at all (only possible with causal and Lq > Lk) has
+  output 0 instead of the NaN that max over an empty set would give.
+* Grouped-query attention maps query head hq to key/value head
+  hq // (Hq // Hkv) (contiguous groups).
+* ALiBi: bias_ij = -slope[hq] * (i_abs - j) with i_abs = i + (Lk - Lq).  The
+  slopes are an input; the oracle takes whatever values the GPU receives.
+"""
+
+import numpy as np
+
+
+def _check(q, k, v, alibi_slopes):
+    if q.ndim != 4 or k.ndim != 4 or v.ndim != 4:
+        raise ValueError("q, k, v must be [B, H, L, D]")
+    B, Hq, Lq, D = q.shape
+    Bk, Hkv, Lk, Dk = k.shape
+    if k.shape != v.shape or Bk != B or Dk != D:
+        raise ValueError("k and v must be [B, Hkv, Lk, D] with q's B and D")
+    if Hkv < 1 or Hq % Hkv != 0:
+        raise ValueError("Hq must be a multiple of Hkv")
+    if alibi_slopes is not None and np.asarray(alibi_slopes).shape != (Hq,):
+        raise ValueError("alibi_slopes must have one value per query head")
+    return B, Hq, Hkv, Lq, Lk, D
+
+
+def scores(q, k, *, scale, causal=False, alibi_slopes=None, b=0, hq=0,
+           rows=None):
+    """Score matrix of one (batch, query head): score_mod(q.k^T) or -inf.
+
+    Returns an array [len(rows), Lk] of float64.  ``rows`` selects query rows
+    (default: all of them); each selected row is computed exactly as it would
+    be in the full matrix.
+    """
+    B, Hq, Lq, D = q.shape
+    Hkv, Lk = k.shape[1], k.shape[2]
+    group = Hq // Hkv
+    hk = hq // group
+    i = np.arange(Lq) if rows is None else np.asarray(rows, dtype=np.int64)
+    qi = np.asarray(q[b, hq], dtype=np.float64)[i]          # [R, D]
+    kk = np.asarray(k[b, hk], dtype=np.float64)              # [Lk, D]
+    p = qi @ kk.T                                            # batch_matmul(q, k, trans_b)
+    i_abs = i[:, None] + (Lk - Lq)                           # bottom-right aligned row index
+    j = np.arange(Lk)[None, :]
+    score = p * float(scale)
+    if alibi_slopes is not None:
+        slope = float(np.asarray(alibi_slopes, dtype=np.float64)[hq])
+        score = score + (-slope) * (i_abs - j)
+    if causal:
+        score = np.where(j <= i_abs, score, -np.inf)
+    return score
+
+
+def softmax_probs(q, k, *, scale, causal=False, alibi_slopes=None, b=0, hq=0,
+                  rows=None):
+    """Probability matrix P = e / s of one (batch, query head), materialised."""
+    score = scores(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes,
+                   b=b, hq=hq, rows=rows)
+    m = score.max(axis=1, keepdims=True)                     # softmax_maxelem
+    empty = ~np.isfinite(m)
+    m = np.where(empty, 0.0, m)
+    e = np.exp(score - m)                                    # softmax_exp
+    s = e.sum(axis=1, keepdims=True)                         # softmax_expsum
+    return np.where(empty, 0.0, e / np.where(empty, 1.0, s))
+
+
+def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, rows=None,
+              heads=None):
+    """O = softmax(q.k^T * scale + bias, masked) . v, in float64.
+
+    q: [B, Hq, Lq, D]; k, v: [B, Hkv, Lk, D]; any real dtype (converted to
+    float64 exactly).  ``alibi_slopes``: None or [Hq] values.  ``rows``:
+    optional query-row indices to compute (others are skipped, not
+    approximated); ``heads``: optional list of (b, hq) pairs to compute.
+    Returns float64 [B, Hq, R, D] where R = Lq or len(rows); rows of skipped
+    heads are NaN.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    B, Hq, Hkv, Lq, Lk, D = _check(q, k, v, alibi_slopes)
+    group = Hq // Hkv
+    R = Lq if rows is None else len(rows)
+    out = np.full((B, Hq, R, D), np.nan)
+    todo = [(b, h) for b in range(B) for h in range(Hq)] if heads is None else heads
+    for b, hq in todo:
+        score = scores(q, k, scale=scale, causal=causal,
+                       alibi_slopes=alibi_slopes, b=b, hq=hq, rows=rows)
+        m = score.max(axis=1, keepdims=True)                 # softmax_maxelem
+        empty = ~np.isfinite(m)                              # row sees no key
+        m = np.where(empty, 0.0, m)
+        e = np.exp(score - m)                                # softmax_exp
+        s = e.sum(axis=1, keepdims=True)                     # softmax_expsum
+        o = e @ v[b, hq // group]                            # batch_matmul(e, v)
+        o = o / np.where(empty, 1.0, s)                      # softmax_norm
+        out[b, hq] = np.where(empty, 0.0, o)
+    return out

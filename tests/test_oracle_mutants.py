@@ -1,0 +1,132 @@
+"""Planted mistakes in the oracle must be caught by its pins (CPU only).
+
+Each mutant is the oracle with one plausible error: a transposed or swapped
+operand, a dropped scale, a wrong bias sign, a wrong causal alignment, a wrong
+GQA head map, a missing repair factor.  The pins in ``test_oracle_pins`` /
+``test_algorithms`` must reject every one of them; this guards against pins
+that are too weak to notice a broken oracle.
+"""
+
+import math
+
+import numpy as np
+
+import oracle
+from oracle import rolling
+from paper_2510_08726_amd.workloads import alibi_slopes
+
+
+def _rand(shape, seed):
+    return np.random.Generator(np.random.PCG64(seed)).standard_normal(shape)
+
+
+def _one_hot_pin(attn):
+    D, Lk = 8, 40
+    rng = np.random.Generator(np.random.PCG64(7))
+    k = rng.standard_normal((1, 1, Lk, D)) * 0.1
+    v = rng.standard_normal((1, 1, Lk, D))
+    q = np.zeros((1, 1, 1, D))
+    q[0, 0, 0, 0] = 1.0
+    k[0, 0, Lk - 1, 0] = 40.0
+    o = attn(q, k, v, scale=1.0)
+    return np.allclose(o[0, 0, 0], v[0, 0, Lk - 1], atol=1e-6)
+
+
+def _logistic_pin(attn):
+    q, k, v = _rand((1, 1, 3, 5), 11), _rand((1, 1, 2, 5), 12), _rand((1, 1, 2, 5), 13)
+    o = attn(q, k, v, scale=0.37)
+    for i in range(3):
+        s = [0.37 * float(q[0, 0, i] @ k[0, 0, j]) for j in range(2)]
+        w0 = 1.0 / (1.0 + math.exp(s[1] - s[0]))
+        if not np.allclose(o[0, 0, i], w0 * v[0, 0, 0] + (1 - w0) * v[0, 0, 1], atol=1e-12):
+            return False
+    return True
+
+
+def _alibi_pin(attn):
+    H, L = 2, 7
+    q, k, v = _rand((1, H, L, 2), 17), _rand((1, H, L, 2), 18), _rand((1, H, L, 2), 19)
+    sl = alibi_slopes(H).double().numpy()
+    o = attn(q, k, v, scale=0.0, causal=True, alibi_slopes=sl)
+    for h in range(H):
+        r = math.exp(-sl[h])
+        for i in range(L):
+            w = np.array([r ** (i - j) for j in range(i + 1)])
+            if not np.allclose(o[0, h, i], (w[:, None] * v[0, h, :i + 1]).sum(0) / w.sum(), atol=1e-12):
+                return False
+    return True
+
+
+def _prefix_mean_pin(attn):
+    q, k, v = _rand((1, 1, 5, 3), 14), _rand((1, 1, 12, 3), 15), _rand((1, 1, 12, 3), 16)
+    o = attn(q, k, v, scale=0.0, causal=True)
+    return all(np.allclose(o[0, 0, i], v[0, 0, :i + 8].mean(0), atol=1e-13) for i in range(5))
+
+
+def _gqa_pin(attn):
+    q, k, v = _rand((1, 4, 6, 4), 23), _rand((1, 2, 6, 4), 24), _rand((1, 2, 6, 4), 25)
+    o = attn(q, k, v, scale=0.3)
+    ref = oracle.attention(q[:, :1], k[:, :1], v[:, :1], scale=0.3)   # hq 0 -> hk 0
+    ref1 = oracle.attention(q[:, 1:2], k[:, :1], v[:, :1], scale=0.3)  # hq 1 -> hk 0
+    return np.allclose(o[:, :1], ref, atol=1e-13) and np.allclose(o[:, 1:2], ref1, atol=1e-13)
+
+
+PINS = [_one_hot_pin, _logistic_pin, _alibi_pin, _prefix_mean_pin, _gqa_pin]
+
+
+def test_true_oracle_passes_every_pin():
+    for pin in PINS:
+        assert pin(oracle.attention), pin.__name__
+
+
+def _caught(mutant):
+    return any(not pin(mutant) for pin in PINS)
+
+
+def test_mutant_qv_instead_of_qk_is_caught():
+    assert _caught(lambda q, k, v, **kw: oracle.attention(q, v, v, **kw))
+
+
+def test_mutant_dropped_scale_is_caught():
+    assert _caught(lambda q, k, v, scale, **kw: oracle.attention(q, k, v, scale=1.0, **kw))
+
+
+def test_mutant_alibi_sign_is_caught():
+    def m(q, k, v, alibi_slopes=None, **kw):
+        sl = None if alibi_slopes is None else -np.asarray(alibi_slopes)
+        return oracle.attention(q, k, v, alibi_slopes=sl, **kw)
+    assert _caught(m)
+
+
+def test_mutant_top_left_causal_is_caught():
+    def m(q, k, v, causal=False, **kw):
+        if not causal:
+            return oracle.attention(q, k, v, **kw)
+        Lq, Lk = q.shape[2], k.shape[2]
+        out = np.zeros(q.shape)
+        for i in range(Lq):                      # row i sees keys 0..i (top-left)
+            out[:, :, i:i + 1] = oracle.attention(q[:, :, i:i + 1], k[:, :, :i + 1], v[:, :, :i + 1], **kw)
+        return out
+    assert _caught(m)
+
+
+def test_mutant_interleaved_gqa_map_is_caught():
+    def m(q, k, v, **kw):
+        G = q.shape[1] // k.shape[1]
+        return oracle.attention(q, np.tile(k, (1, G, 1, 1)), np.tile(v, (1, G, 1, 1)), **kw)
+    assert _caught(m)
+
+
+def test_mutant_missing_repair_factor_is_caught():
+    """Rolling update without h (alpha = 1) breaks Theorem 1."""
+    q, k, v = _rand((1, 1, 4, 8), 1), _rand((1, 1, 64, 8), 2), _rand((1, 1, 64, 8), 3)
+    ref = oracle.attention(q, k, v, scale=0.5)[0, 0]
+    saved = rolling._repair
+    try:
+        rolling._repair = lambda prev, cur: np.ones_like(cur)
+        bad = rolling.rolling_update_attention(q, k, v, scale=0.5, block_n=16)
+    finally:
+        rolling._repair = saved
+    assert not np.allclose(bad, ref, atol=1e-6)
+    good = rolling.rolling_update_attention(q, k, v, scale=0.5, block_n=16)
+    np.testing.assert_allclose(good, ref, atol=1e-12)
