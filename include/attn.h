@@ -1,0 +1,144 @@
+/*
+ * attn.h — fused scaled-dot-product attention for AMD Instinct MI355X (gfx950).
+ *
+ * The operation is plain attention as the paper defines it (Eq. attention in
+ * the appendix "Additional Example Operators" and the compute definition of the
+ * appendix figure "Compute definition for the attention operator"):
+ *
+ *     S = Q K^T * scale + bias          (masked entries are -inf)
+ *     O = softmax_rows(S) V             (exp rounded to the input dtype before P.V)
+ *
+ * computed without ever materialising S:
+ *   - attn_fwd    is the kernel that "rolling update" (Section "Rolling Update",
+ *                 Algorithm 1, Eq. fixed-recurrent) produces from that
+ *                 definition: one pass over key tiles, the running max / sum /
+ *                 P.V state repaired by h(t, r, r') = t * exp(r - r') whenever
+ *                 the running max moves;
+ *   - attn_decode is what "split-k update" (Section "Split-K Update",
+ *                 Algorithm 2, Eq. su:rewrite) produces for one query token:
+ *                 independent local nests over key chunks write partial
+ *                 (O, max, sum) triples, and a global nest combines them with
+ *                 the same repair factor.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensor pointers are DEVICE pointers to contiguous row-major tensors laid
+ *    out [B, H, L, D] (D fastest).  Q, K, V and O share one element type
+ *    (attn_dtype).  Q and O have Hq heads, K and V have Hkv heads.
+ *  - Grouped-query attention: Hq must be a multiple of Hkv; query head hq reads
+ *    key/value head hq / (Hq / Hkv) (contiguous groups).  Hkv == Hq is
+ *    multi-head attention.
+ *  - scale multiplies Q K^T only (callers normally pass 1/sqrt(D)); the ALiBi
+ *    bias is added after scaling: bias[i][j] = -alibi_slopes[hq] * (i + Lk - Lq - j).
+ *    alibi_slopes is a DEVICE array of Hq floats, or NULL for no bias.
+ *  - causal masking is aligned bottom-right: query row i sees key j iff
+ *    j <= i + (Lk - Lq).  With Lq == Lk that is j <= i.  A row that sees no
+ *    key (only possible when Lq > Lk) produces zeros.
+ *  - Accumulation and the softmax state are fp32; the output is rounded to
+ *    the input type (round to nearest even).
+ *  - Ownership: the caller allocates and frees every buffer (including the
+ *    decode workspace).  The library holds no device memory and no global
+ *    mutable state apart from a thread-local copy of the last HIP error.
+ *  - Asynchrony: work is enqueued on `stream` and the call returns without
+ *    synchronising.  Argument errors are detected on the host before
+ *    anything is enqueued; in that case nothing runs and no HIP call is made.
+ *  - O must not alias Q, K or V.  Each call is deterministic: the same inputs
+ *    and arguments give bitwise identical outputs (no atomics).
+ *  - Return value: ATTN_OK or a negative attn_status.
+ */
+#ifndef ATTN_H
+#define ATTN_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ATTN_F16 = 0,  /* IEEE binary16 */
+  ATTN_BF16 = 1  /* bfloat16 */
+} attn_dtype;
+
+typedef enum {
+  ATTN_OK = 0,
+  ATTN_ERR_NULL = -1,        /* a required pointer is NULL */
+  ATTN_ERR_SHAPE = -2,       /* a size is < 1, Hq % Hkv != 0, num_splits < 0, or a size overflows */
+  ATTN_ERR_UNSUPPORTED = -3, /* head dim not 64 or 128, or unknown dtype */
+  ATTN_ERR_WORKSPACE = -4,   /* decode workspace smaller than attn_decode_workspace_bytes() */
+  ATTN_ERR_HIP = -5          /* a HIP launch failed; see attn_last_hip_error() */
+} attn_status;
+
+/*
+ * Prefill / general attention (rolling update).
+ *
+ *   Q [B, Hq, Lq, D], K and V [B, Hkv, Lk, D], O [B, Hq, Lq, D]   (device)
+ *   B, Hq, Hkv, Lq, Lk >= 1; Hq % Hkv == 0; D in {64, 128}
+ *   causal  0 or 1 (non-zero means 1)
+ *   scale   finite float
+ *   alibi_slopes  device float[Hq] or NULL
+ *
+ * Errors: ATTN_ERR_NULL if Q, K, V or O is NULL; ATTN_ERR_SHAPE for bad sizes;
+ * ATTN_ERR_UNSUPPORTED for D or dtype; ATTN_ERR_HIP if the launch fails.
+ */
+int attn_fwd(const void* Q, const void* K, const void* V, void* O,
+             int B, int Hq, int Hkv, int Lq, int Lk, int D,
+             int causal, float scale, const float* alibi_slopes,
+             attn_dtype dtype, hipStream_t stream);
+
+/*
+ * Bytes of decode workspace needed for (B, Hq, D, num_splits), num_splits >= 1
+ * (resolve 0 with attn_decode_num_splits first).  Returns 0 for invalid sizes.
+ *
+ * Workspace layout (fp32, offsets in floats, n = B*Hq*num_splits): the local
+ * nests' results of the split-k update (Fig. su-result), in natural-log units,
+ * for head row r = b*Hq + hq and chunk s:
+ *   o_l   at [0, n*D)        o_l[(r*num_splits + s)*D + d]   unnormalised sum of
+ *                                                            exp(score - max_l) * V
+ *   max_l at [n*D, n*D + n)  max_l[r*num_splits + s]         chunk max of the scores
+ *   sum_l at [n*D + n, n*D + 2n) sum_l[r*num_splits + s]     sum of exp(score - max_l)
+ * A chunk with no key has max_l = -inf, sum_l = 0, o_l = 0.
+ */
+size_t attn_decode_workspace_bytes(int B, int Hq, int D, int num_splits);
+
+/*
+ * The number of key chunks attn_decode uses when num_splits == 0 (the library
+ * heuristic: enough workgroups to fill the GPU, chunks of at least 256 keys).
+ * Returns a value >= 1, or 0 for invalid sizes.
+ */
+int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D);
+
+/*
+ * Single-token decode (split-k update).
+ *
+ *   Q [B, Hq, 1, D], K and V [B, Hkv, Lk, D], O [B, Hq, 1, D]   (device)
+ *   The query is the token at position Lk - 1, so every key is visible (the
+ *   causal mask is a no-op).  alibi_slopes as for attn_fwd, with i = Lk - 1.
+ *   num_splits  >= 1 chunks of ceil(Lk / num_splits) keys (the last chunk may
+ *               be short, chunks past Lk are empty), or 0 for the heuristic.
+ *   workspace   device buffer of at least attn_decode_workspace_bytes(B, Hq,
+ *               D, resolved num_splits) bytes, 16-byte aligned; its contents
+ *               after the call are the local partials described above.
+ *
+ * Two kernels run on `stream`: the local split kernel, then the combine.
+ * Errors: ATTN_ERR_NULL (Q, K, V, O or workspace NULL), ATTN_ERR_SHAPE,
+ * ATTN_ERR_UNSUPPORTED, ATTN_ERR_WORKSPACE, ATTN_ERR_HIP.
+ */
+int attn_decode(const void* Q, const void* K, const void* V, void* O,
+                int B, int Hq, int Hkv, int Lk, int D,
+                float scale, const float* alibi_slopes, int num_splits,
+                void* workspace, size_t workspace_bytes,
+                attn_dtype dtype, hipStream_t stream);
+
+/* Static, human-readable name of an attn_status value. */
+const char* attn_status_string(int status);
+
+/* The hipError_t of the last ATTN_ERR_HIP returned on this thread (0 if none). */
+int attn_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTN_H */

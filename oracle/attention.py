@@ -97,16 +97,13 @@ def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, rows=None,
               heads=None):
     """O = softmax(q.k^T * scale + bias, masked) . v, in float64.
 
-    q: [B, Hq, Lq, D]; k, v: [B, Hkv, Lk, D]; any real dtype (converted to
-    float64 exactly).  ``alibi_slopes``: None or [Hq] values.  ``rows``:
+    q: [B, Hq, Lq, D]; k, v: [B, Hkv, Lk, D]; numpy arrays of any real dtype,
+    converted to float64 exactly one (batch, head) slice at a time.  ``alibi_slopes``: None or [Hq] values.  ``rows``:
     optional query-row indices to compute (others are skipped, not
     approximated); ``heads``: optional list of (b, hq) pairs to compute.
     Returns float64 [B, Hq, R, D] where R = Lq or len(rows); rows of skipped
     heads are NaN.
     """
-    q = np.asarray(q, dtype=np.float64)
-    k = np.asarray(k, dtype=np.float64)
-    v = np.asarray(v, dtype=np.float64)
     B, Hq, Hkv, Lq, Lk, D = _check(q, k, v, alibi_slopes)
     group = Hq // Hkv
     R = Lq if rows is None else len(rows)
@@ -120,7 +117,7 @@ def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, rows=None,
         m = np.where(empty, 0.0, m)
         e = np.exp(score - m)                                # softmax_exp
         s = e.sum(axis=1, keepdims=True)                     # softmax_expsum
-        o = e @ v[b, hq // group]                            # batch_matmul(e, v)
+        o = e @ np.asarray(v[b, hq // group], dtype=np.float64)  # batch_matmul(e, v)
         o = o / np.where(empty, 1.0, s)                      # softmax_norm
         out[b, hq] = np.where(empty, 0.0, o)
     return out

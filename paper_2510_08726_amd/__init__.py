@@ -1,0 +1,188 @@
+"""Fused attention for AMD Instinct MI355X (gfx950) — Python binding of libattn.so.
+
+A thin ctypes layer over the C ABI declared in ``include/attn.h``: the
+functions below have the same names as the C entry points and only marshal
+arguments (device pointers, sizes, the current HIP stream).  Every step of the
+computation runs in the HIP kernels of ``libattn.so``; PyTorch only provides
+device memory and streams.  There is no fallback: if the library is missing
+or a call fails, an exception is raised.
+"""
+
+import ctypes
+import math
+import os
+
+import torch
+
+__all__ = [
+    "attn_fwd", "attn_decode", "attn_decode_workspace_bytes", "attn_decode_num_splits",
+    "attn_status_string", "attn_last_hip_error", "library_path", "load_library", "AttnError",
+    "ATTN_OK", "ATTN_ERR_NULL", "ATTN_ERR_SHAPE", "ATTN_ERR_UNSUPPORTED", "ATTN_ERR_WORKSPACE",
+    "ATTN_ERR_HIP",
+]
+
+ATTN_OK = 0
+ATTN_ERR_NULL = -1
+ATTN_ERR_SHAPE = -2
+ATTN_ERR_UNSUPPORTED = -3
+ATTN_ERR_WORKSPACE = -4
+ATTN_ERR_HIP = -5
+
+ATTN_F16 = 0
+ATTN_BF16 = 1
+_DTYPE_CODE = {torch.float16: ATTN_F16, torch.bfloat16: ATTN_BF16}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+
+class AttnError(RuntimeError):
+    """A call into libattn.so returned an error status."""
+
+    def __init__(self, status, msg):
+        super().__init__(msg)
+        self.status = status
+
+
+def library_path():
+    return os.path.join(_HERE, "libattn.so")
+
+
+def load_library():
+    """Load (once) and return the ctypes handle of libattn.so; raises if absent."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is not built; run `python -c 'import __graft_entry__ as g; g.build()'` "
+            "or `python paper_2510_08726_amd/build.py` first")
+    lib = ctypes.CDLL(path)
+    vp, ci, cf, cs = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, vp, ci, vp]
+    lib.attn_fwd.restype = ci
+    lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, ci, vp, cs, ci, vp]
+    lib.attn_decode.restype = ci
+    lib.attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci]
+    lib.attn_decode_workspace_bytes.restype = cs
+    lib.attn_decode_num_splits.argtypes = [ci, ci, ci, ci, ci]
+    lib.attn_decode_num_splits.restype = ci
+    lib.attn_status_string.argtypes = [ci]
+    lib.attn_status_string.restype = ctypes.c_char_p
+    lib.attn_last_hip_error.argtypes = []
+    lib.attn_last_hip_error.restype = ci
+    _LIB = lib
+    return lib
+
+
+def attn_status_string(status):
+    return load_library().attn_status_string(int(status)).decode()
+
+
+def attn_last_hip_error():
+    return load_library().attn_last_hip_error()
+
+
+def _check(rc):
+    if rc != ATTN_OK:
+        msg = attn_status_string(rc)
+        if rc == ATTN_ERR_HIP:
+            msg += f" (hipError_t {attn_last_hip_error()})"
+        raise AttnError(rc, msg)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _require(cond, msg):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _check_tensors(q, k, v, slopes):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _require(t.is_cuda, f"{name} must be a GPU tensor")
+        _require(t.is_contiguous(), f"{name} must be contiguous [B, H, L, D]")
+        _require(t.dim() == 4, f"{name} must be 4-D [B, H, L, D]")
+    _require(q.dtype == k.dtype == v.dtype, "q, k, v must share one dtype")
+    _require(q.dtype in _DTYPE_CODE, "dtype must be float16 or bfloat16")
+    _require(k.shape == v.shape, "k and v must have the same shape")
+    if slopes is not None:
+        _require(slopes.is_cuda and slopes.dtype == torch.float32 and slopes.is_contiguous(),
+                 "alibi_slopes must be a contiguous float32 GPU tensor")
+        _require(slopes.numel() == q.shape[1], "alibi_slopes needs one value per query head")
+
+
+def attn_fwd(q, k, v, o=None, *, causal=False, scale=None, alibi_slopes=None, stream=None):
+    """O = softmax(Q K^T * scale + bias) V by the fused prefill kernel.
+
+    q [B, Hq, Lq, D], k and v [B, Hkv, Lk, D] (float16 or bfloat16, contiguous,
+    on the GPU); ``o`` is written if given, else allocated.  ``scale``
+    defaults to 1/sqrt(D).  Returns ``o``.
+    """
+    _check_tensors(q, k, v, alibi_slopes)
+    B, Hq, Lq, D = q.shape
+    Hkv, Lk = k.shape[1], k.shape[2]
+    _require(k.shape[0] == B and k.shape[3] == D, "k/v batch and head dim must match q")
+    if o is None:
+        o = torch.empty_like(q)
+    _require(o.shape == q.shape and o.dtype == q.dtype and o.is_contiguous() and o.is_cuda,
+             "o must be a contiguous GPU tensor shaped like q")
+    sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    lib = load_library()
+    _check(lib.attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lq, Lk, D,
+                        int(bool(causal)), sc, _ptr(alibi_slopes), _DTYPE_CODE[q.dtype],
+                        _stream(stream)))
+    return o
+
+
+def attn_decode_workspace_bytes(B, Hq, D, num_splits):
+    return load_library().attn_decode_workspace_bytes(B, Hq, D, num_splits)
+
+
+def attn_decode_num_splits(B, Hq, Hkv, Lk, D):
+    return load_library().attn_decode_num_splits(B, Hq, Hkv, Lk, D)
+
+
+def attn_decode(q, k, v, o=None, *, scale=None, alibi_slopes=None, num_splits=0,
+                workspace=None, stream=None):
+    """Single-token decode by split-k: q [B, Hq, 1, D] against k, v [B, Hkv, Lk, D].
+
+    ``num_splits`` = 0 lets the library choose.  ``workspace`` (uint8 GPU
+    tensor) is allocated when not given.  Returns ``o`` [B, Hq, 1, D].
+    """
+    _check_tensors(q, k, v, alibi_slopes)
+    B, Hq, Lq, D = q.shape
+    _require(Lq == 1, "decode takes one query token (q.shape[2] == 1)")
+    Hkv, Lk = k.shape[1], k.shape[2]
+    _require(k.shape[0] == B and k.shape[3] == D, "k/v batch and head dim must match q")
+    if o is None:
+        o = torch.empty_like(q)
+    _require(o.shape == q.shape and o.dtype == q.dtype and o.is_contiguous() and o.is_cuda,
+             "o must be a contiguous GPU tensor shaped like q")
+    lib = load_library()
+    S = num_splits if num_splits else lib.attn_decode_num_splits(B, Hq, Hkv, Lk, D)
+    need = lib.attn_decode_workspace_bytes(B, Hq, D, max(S, 1))
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    _check(lib.attn_decode(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lk, D, sc,
+                           _ptr(alibi_slopes), int(num_splits), _ptr(workspace),
+                           workspace.numel() * workspace.element_size(), _DTYPE_CODE[q.dtype],
+                           _stream(stream)))
+    return o
+
+
+def decode_partials(workspace, B, Hq, D, num_splits):
+    """View the decode workspace as (o_l [B,Hq,S,D], max_l [B,Hq,S], sum_l [B,Hq,S]) fp32."""
+    n = B * Hq * num_splits
+    f = workspace.view(torch.float32)
+    return (f[:n * D].view(B, Hq, num_splits, D), f[n * D:n * D + n].view(B, Hq, num_splits),
+            f[n * D + n:n * D + 2 * n].view(B, Hq, num_splits))

@@ -1,0 +1,148 @@
+// C ABI of the fused-attention library: argument validation on the host,
+// dispatch to the gfx950 kernels, error reporting.  Every check runs before
+// any HIP call, so a rejected call enqueues nothing.
+
+#include <cmath>
+#include <cstdint>
+#include <limits>
+
+#include "../../include/attn.h"
+#include "launch.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int64_t kMaxGrid = std::numeric_limits<int32_t>::max();
+constexpr int kMinChunk = 256;    // keys per decode chunk chosen by the heuristic
+constexpr int kTargetBlocks = 4096;
+
+bool shape_ok(int B, int Hq, int Hkv, int Lq, int Lk) {
+  return B >= 1 && Hq >= 1 && Hkv >= 1 && Lq >= 1 && Lk >= 1 && Hq % Hkv == 0;
+}
+
+bool dims_supported(int D, attn_dtype dtype) {
+  return (D == 64 || D == 128) && (dtype == ATTN_F16 || dtype == ATTN_BF16);
+}
+
+// Element counts must stay addressable and the grids within 2^31 - 1 blocks.
+bool sizes_fit(int B, int Hq, int Hkv, int Lq, int Lk, int D) {
+  const int64_t q = (int64_t)B * Hq * Lq * D;
+  const int64_t k = (int64_t)B * Hkv * Lk * D;
+  return q < (int64_t(1) << 40) && k < (int64_t(1) << 40);
+}
+
+int hip_fail(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return ATTN_ERR_HIP;
+}
+
+int gqa_heads_per_block(int group) {
+  if (group % 8 == 0) return 8;
+  if (group % 4 == 0) return 4;
+  if (group % 2 == 0) return 2;
+  return 1;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* attn_status_string(int status) {
+  switch (status) {
+    case ATTN_OK: return "ATTN_OK: success";
+    case ATTN_ERR_NULL: return "ATTN_ERR_NULL: a required pointer is NULL";
+    case ATTN_ERR_SHAPE: return "ATTN_ERR_SHAPE: invalid sizes (need B,Hq,Hkv,Lq,Lk >= 1, Hq % Hkv == 0, num_splits >= 0, finite scale)";
+    case ATTN_ERR_UNSUPPORTED: return "ATTN_ERR_UNSUPPORTED: head dim must be 64 or 128 and dtype ATTN_F16 or ATTN_BF16";
+    case ATTN_ERR_WORKSPACE: return "ATTN_ERR_WORKSPACE: decode workspace too small";
+    case ATTN_ERR_HIP: return "ATTN_ERR_HIP: a HIP launch failed (see attn_last_hip_error)";
+    default: return "unknown attn_status";
+  }
+}
+
+int attn_last_hip_error(void) { return g_last_hip_error; }
+
+int attn_fwd(const void* Q, const void* K, const void* V, void* O,
+             int B, int Hq, int Hkv, int Lq, int Lk, int D,
+             int causal, float scale, const float* alibi_slopes,
+             attn_dtype dtype, hipStream_t stream) {
+  if (!Q || !K || !V || !O) return ATTN_ERR_NULL;
+  if (!shape_ok(B, Hq, Hkv, Lq, Lk) || !std::isfinite(scale)) return ATTN_ERR_SHAPE;
+  if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
+  if (!sizes_fit(B, Hq, Hkv, Lq, Lk, D)) return ATTN_ERR_SHAPE;
+  const int bm = attn::prefill_block_rows();
+  const int64_t nqb = ((int64_t)Lq + bm - 1) / bm;
+  if (nqb * B * Hq > kMaxGrid) return ATTN_ERR_SHAPE;
+
+  attn::PrefillParams p{};
+  p.q = Q; p.k = K; p.v = V; p.o = O;
+  p.slopes = alibi_slopes;
+  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Lq = Lq; p.Lk = Lk; p.D = D;
+  p.group = Hq / Hkv;
+  p.causal = causal ? 1 : 0;
+  p.bf16 = dtype == ATTN_BF16;
+  if (alibi_slopes) {
+    p.c = scale * kLog2e;
+    p.qsign = 0;
+  } else {
+    p.c = std::fabs(scale) * kLog2e;
+    p.qsign = std::signbit(scale) ? 0x80008000u : 0u;
+  }
+  p.nqb = (int)nqb;
+  hipError_t e = attn::launch_prefill(p, stream);
+  return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
+int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D) {
+  if (!shape_ok(B, Hq, Hkv, 1, Lk) || (D != 64 && D != 128)) return 0;
+  const int64_t groups = Hq / Hkv / gqa_heads_per_block(Hq / Hkv);
+  const int64_t units = (int64_t)B * Hkv * groups;
+  int64_t s = (kTargetBlocks + units - 1) / units;
+  const int64_t smax = ((int64_t)Lk + kMinChunk - 1) / kMinChunk;
+  if (s > smax) s = smax;
+  if (s < 1) s = 1;
+  return (int)s;
+}
+
+size_t attn_decode_workspace_bytes(int B, int Hq, int D, int num_splits) {
+  if (B < 1 || Hq < 1 || num_splits < 1 || (D != 64 && D != 128)) return 0;
+  const size_t n = (size_t)B * Hq * num_splits;
+  const size_t bytes = n * (size_t)(D + 2) * sizeof(float);
+  return (bytes + 255) & ~(size_t)255;
+}
+
+int attn_decode(const void* Q, const void* K, const void* V, void* O,
+                int B, int Hq, int Hkv, int Lk, int D,
+                float scale, const float* alibi_slopes, int num_splits,
+                void* workspace, size_t workspace_bytes,
+                attn_dtype dtype, hipStream_t stream) {
+  if (!Q || !K || !V || !O || !workspace) return ATTN_ERR_NULL;
+  if (!shape_ok(B, Hq, Hkv, 1, Lk) || num_splits < 0 || !std::isfinite(scale)) return ATTN_ERR_SHAPE;
+  if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
+  if (!sizes_fit(B, Hq, Hkv, 1, Lk, D)) return ATTN_ERR_SHAPE;
+  const int S = num_splits ? num_splits : attn_decode_num_splits(B, Hq, Hkv, Lk, D);
+  const int group = Hq / Hkv;
+  const int64_t nblocks = (int64_t)S * (group / gqa_heads_per_block(group)) * Hkv * B;
+  if (nblocks > kMaxGrid || (int64_t)B * Hq > kMaxGrid) return ATTN_ERR_SHAPE;
+  const size_t need = attn_decode_workspace_bytes(B, Hq, D, S);
+  if (workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 15)) return ATTN_ERR_WORKSPACE;
+
+  attn::DecodeParams p{};
+  p.q = Q; p.k = K; p.v = V; p.o = O;
+  p.slopes = alibi_slopes;
+  const size_t n = (size_t)B * Hq * S;
+  p.ws_o = static_cast<float*>(workspace);
+  p.ws_m = p.ws_o + n * D;
+  p.ws_l = p.ws_m + n;
+  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Lk = Lk; p.D = D;
+  p.group = group;
+  p.splits = S;
+  p.chunk = (Lk + S - 1) / S;
+  p.bf16 = dtype == ATTN_BF16;
+  p.c = scale * kLog2e;
+  hipError_t e = attn::launch_decode(p, stream);
+  return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
+}  // extern "C"

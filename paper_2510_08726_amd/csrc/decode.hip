@@ -1,0 +1,266 @@
+// Single-token decode for gfx950: the two loop nests that split-k update
+// (Section "Split-K Update", Algorithm 2, Fig. su-result) produces from the
+// attention definition when the key reduction is privatised into chunks.
+//
+//  split kernel    one workgroup per (chunk s, key/value head, batch, query
+//                  head group).  It streams its chunk of K and V exactly once
+//                  from HBM and runs the LOCAL nests for every query head
+//                  that shares the key/value head (grouped-query attention):
+//                  chunk max, exp-sum and unnormalised P.V.  These partials
+//                  are not repaired; they are written to the workspace.
+//  combine kernel  the GLOBAL nests: max over chunks, then every partial is
+//                  rescaled by exp(max_l - max_g) (the repair function on the
+//                  right of the reducer, Eq. su:rewrite) and summed.
+//
+// Decode moves ~1 flop per byte, so the split kernel is an HBM stream: each
+// key row (D * 2 bytes) is read by D / 8 lanes with 16-byte loads, the dot
+// products use v_dot2 on packed pairs, and the per-key partial dot is
+// reduced across those lanes with DPP.  Inside a workgroup every lane group
+// keeps its own online-softmax state over its keys; the groups are merged
+// once at the end.
+
+#include "kernel_common.h"
+#include "launch.h"
+
+namespace attn {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;  // keys per lane group per step (loads in flight)
+
+// Sum over aligned groups of LPK lanes (LPK = 8 or 16); every lane of the
+// group receives the sum.  quad_perm swaps lanes ^1 and ^2, row_half_mirror
+// pairs the two quads of an 8-lane half row, row_mirror the two halves of a
+// 16-lane row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+
+template <int LPK>
+__device__ __forceinline__ float group_sum(float x) {
+  x += dpp_move<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp_move<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp_move<0x141>(x);  // row_half_mirror
+  if (LPK == 16) x += dpp_move<0x140>(x);  // row_mirror
+  return x;
+}
+
+template <int D, typename T, int GH, bool ALIBI>
+__global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) {
+  typedef Elem<T> E;
+  constexpr int LPK = D / 8;               // lanes per key row
+  constexpr int GPW = 64 / LPK;            // lane groups per wave
+  constexpr int NG = GPW * (kThreads / 64);  // lane groups per workgroup
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int lig = lane % LPK;              // lane within its group: dims 8 lig .. 8 lig + 7
+  const int grp = wave * GPW + lane / LPK;  // group index in the workgroup
+
+  const int S = p.splits;
+  const int ngrp = p.group / GH;
+  int bid = blockIdx.x;
+  const int s = bid % S;  bid /= S;
+  const int hg = bid % ngrp;  bid /= ngrp;
+  const int hk = bid % p.Hkv;
+  const int b = bid / p.Hkv;
+  const int hq0 = hk * p.group + hg * GH;   // first query head of this workgroup
+  const int Lk = p.Lk;
+  const int ks = min(s * p.chunk, Lk);
+  const int ke = min(ks + p.chunk, Lk);
+
+  const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)(b * p.Hkv + hk) * Lk * D + 8 * lig;
+  const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)(b * p.Hkv + hk) * Lk * D + 8 * lig;
+
+  // Query rows of the GH heads (packed pairs), the scale is applied after the dot.
+  uint4 qv[GH];
+  float sl2[GH];
+#pragma unroll
+  for (int g = 0; g < GH; ++g) {
+    const T* qp = reinterpret_cast<const T*>(p.q) + ((size_t)b * p.Hq + hq0 + g) * D + 8 * lig;
+    qv[g] = *reinterpret_cast<const uint4*>(qp);
+    sl2[g] = ALIBI ? p.slopes[hq0 + g] * kLog2e : 0.f;
+  }
+
+  float m[GH], l[GH], o[GH][8];
+#pragma unroll
+  for (int g = 0; g < GH; ++g) {
+    m[g] = kNegInf;
+    l[g] = 0.f;
+#pragma unroll
+    for (int d = 0; d < 8; ++d) o[g][d] = 0.f;
+  }
+
+  const float c = p.c;
+  for (int base = ks; base < ke; base += NG * kUnroll) {
+    uint4 kr[kUnroll], vr[kUnroll];
+    int key[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      key[u] = base + u * NG + grp;
+      const bool ok = key[u] < ke;
+      kr[u] = ok ? *reinterpret_cast<const uint4*>(kp + (size_t)key[u] * D) : make_uint4(0, 0, 0, 0);
+      vr[u] = ok ? *reinterpret_cast<const uint4*>(vp + (size_t)key[u] * D) : make_uint4(0, 0, 0, 0);
+    }
+    float vf[kUnroll][8];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      vf[u][0] = E::lo(vr[u].x); vf[u][1] = E::hi(vr[u].x);
+      vf[u][2] = E::lo(vr[u].y); vf[u][3] = E::hi(vr[u].y);
+      vf[u][4] = E::lo(vr[u].z); vf[u][5] = E::hi(vr[u].z);
+      vf[u][6] = E::lo(vr[u].w); vf[u][7] = E::hi(vr[u].w);
+    }
+#pragma unroll
+    for (int g = 0; g < GH; ++g) {
+      float sc[kUnroll];
+      float mt = kNegInf;
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        float part = E::dot2(qv[g].x, kr[u].x, 0.f);
+        part = E::dot2(qv[g].y, kr[u].y, part);
+        part = E::dot2(qv[g].z, kr[u].z, part);
+        part = E::dot2(qv[g].w, kr[u].w, part);
+        float x = group_sum<LPK>(part) * c;
+        if (ALIBI) x = __builtin_fmaf(sl2[g], (float)(key[u] - (Lk - 1)), x);
+        sc[u] = key[u] < ke ? x : kNegInf;
+        mt = fmaxf(mt, sc[u]);
+      }
+      const float mnew = fmaxf(m[g], mt);
+      if (mnew != kNegInf) {
+        const float alpha = m[g] == kNegInf ? 0.f : fast_exp2(m[g] - mnew);
+        float ps = 0.f;
+        float pu[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          pu[u] = sc[u] == kNegInf ? 0.f : fast_exp2(sc[u] - mnew);
+          ps += pu[u];
+        }
+        l[g] = __builtin_fmaf(l[g], alpha, ps);
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+          float acc = o[g][d] * alpha;
+#pragma unroll
+          for (int u = 0; u < kUnroll; ++u) acc = __builtin_fmaf(pu[u], vf[u][d], acc);
+          o[g][d] = acc;
+        }
+        m[g] = mnew;
+      }
+    }
+  }
+
+  // Merge the lane groups of each wave (lanes LPK apart), then the 4 waves
+  // through LDS.  All in log2 units.
+  __shared__ float sh_m[4][GH];
+  __shared__ float sh_l[4][GH];
+  __shared__ float sh_o[4][GH][D];
+#pragma unroll
+  for (int g = 0; g < GH; ++g) {
+    float M = m[g];
+#pragma unroll
+    for (int x = LPK; x < 64; x <<= 1) M = fmaxf(M, __shfl_xor(M, x, 64));
+    const float w = (m[g] == kNegInf) ? 0.f : fast_exp2(m[g] - M);
+    float L = l[g] * w;
+#pragma unroll
+    for (int x = LPK; x < 64; x <<= 1) L += __shfl_xor(L, x, 64);
+    float ov[8];
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      float v = o[g][d] * w;
+#pragma unroll
+      for (int x = LPK; x < 64; x <<= 1) v += __shfl_xor(v, x, 64);
+      ov[d] = v;
+    }
+    if (lane < LPK) {
+#pragma unroll
+      for (int d = 0; d < 8; ++d) sh_o[wave][g][8 * lig + d] = ov[d];
+      if (lig == 0) {
+        sh_m[wave][g] = M;
+        sh_l[wave][g] = L;
+      }
+    }
+  }
+  __syncthreads();
+
+  const size_t rowbase = (size_t)b * p.Hq + hq0;
+  for (int idx = tid; idx < GH * D; idx += kThreads) {
+    const int g = idx / D, d = idx % D;
+    float M = kNegInf;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, sh_m[w][g]);
+    float L = 0.f, acc = 0.f;
+    if (M != kNegInf) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float mw = sh_m[w][g];
+        const float f = mw == kNegInf ? 0.f : fast_exp2(mw - M);
+        L = __builtin_fmaf(sh_l[w][g], f, L);
+        acc = __builtin_fmaf(sh_o[w][g][d], f, acc);
+      }
+    }
+    const size_t slot = (rowbase + g) * S + s;
+    p.ws_o[slot * D + d] = acc;
+    if (d == 0) {
+      p.ws_m[slot] = M == kNegInf ? kNegInf : M * kLn2;   // natural-log units
+      p.ws_l[slot] = L;
+    }
+  }
+}
+
+// Global nests: one workgroup per (batch, query head), one thread per head dim.
+template <int D, typename T>
+__global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams p) {
+  typedef Elem<T> E;
+  const int row = blockIdx.x;   // b * Hq + hq
+  const int d = threadIdx.x;
+  const int S = p.splits;
+  const float* mp = p.ws_m + (size_t)row * S;
+  const float* lp = p.ws_l + (size_t)row * S;
+  const float* op = p.ws_o + (size_t)row * S * D + d;
+  float M = kNegInf;
+  for (int s = 0; s < S; ++s) M = fmaxf(M, mp[s]);
+  float L = 0.f, acc = 0.f;
+  if (M != kNegInf) {
+    for (int s = 0; s < S; ++s) {
+      const float ms = mp[s];
+      const float w = ms == kNegInf ? 0.f : fast_exp2((ms - M) * kLog2e);
+      L = __builtin_fmaf(w, lp[s], L);
+      acc = __builtin_fmaf(w, op[(size_t)s * D], acc);
+    }
+  }
+  const float out = L > 0.f ? acc / L : 0.f;
+  T* dst = reinterpret_cast<T*>(p.o) + (size_t)row * D + d;
+  *dst = (T)out;
+}
+
+template <int D, typename T, int GH>
+hipError_t launch_split(const DecodeParams& p, hipStream_t stream) {
+  const int nblocks = p.splits * (p.group / GH) * p.Hkv * p.B;
+  if (p.slopes)
+    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, true>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, false>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((decode_combine_kernel<D, T>), dim3(p.B * p.Hq), dim3(D), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int D, typename T>
+hipError_t launch_g(const DecodeParams& p, hipStream_t stream) {
+  if (p.group % 8 == 0) return launch_split<D, T, 8>(p, stream);
+  if (p.group % 4 == 0) return launch_split<D, T, 4>(p, stream);
+  if (p.group % 2 == 0) return launch_split<D, T, 2>(p, stream);
+  return launch_split<D, T, 1>(p, stream);
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
+  if (p.D == 64) return p.bf16 ? launch_g<64, __bf16>(p, stream) : launch_g<64, _Float16>(p, stream);
+  return p.bf16 ? launch_g<128, __bf16>(p, stream) : launch_g<128, _Float16>(p, stream);
+}
+
+}  // namespace attn

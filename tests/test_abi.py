@@ -1,0 +1,121 @@
+"""The C ABI on the host: the library loads, exports every declared symbol and
+rejects bad arguments before any HIP call (no GPU needed, no compute call).
+
+Pointers passed here are never dereferenced: every call below fails host-side
+validation, which runs before anything is enqueued.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2510_08726_amd as pa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = ctypes.c_void_p(0x1000)   # non-NULL, never dereferenced on these paths
+NULL = None
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pa.library_path()):
+        import __graft_entry__
+        __graft_entry__.build()
+    return pa.load_library()
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "attn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(attn_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert {"attn_fwd", "attn_decode", "attn_decode_workspace_bytes",
+            "attn_decode_num_splits", "attn_status_string", "attn_last_hip_error"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5):
+        s = pa.attn_status_string(code)
+        assert s.startswith("ATTN_")
+    assert "unknown" in pa.attn_status_string(-99)
+    assert pa.attn_last_hip_error() == 0
+
+
+def fwd(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=1, Hq=2, Hkv=2, Lq=8, Lk=8, D=64, causal=0,
+        scale=0.125, slopes=NULL, dtype=0):
+    return lib.attn_fwd(q, k, v, o, B, Hq, Hkv, Lq, Lk, D, causal, scale, slopes, dtype, NULL)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=NULL), pa.ATTN_ERR_NULL), (dict(k=NULL), pa.ATTN_ERR_NULL),
+    (dict(v=NULL), pa.ATTN_ERR_NULL), (dict(o=NULL), pa.ATTN_ERR_NULL),
+    (dict(B=0), pa.ATTN_ERR_SHAPE), (dict(Hq=0), pa.ATTN_ERR_SHAPE),
+    (dict(Hkv=0), pa.ATTN_ERR_SHAPE), (dict(Lq=0), pa.ATTN_ERR_SHAPE),
+    (dict(Lk=-3), pa.ATTN_ERR_SHAPE), (dict(Hq=6, Hkv=4), pa.ATTN_ERR_SHAPE),
+    (dict(scale=float("nan")), pa.ATTN_ERR_SHAPE), (dict(scale=float("inf")), pa.ATTN_ERR_SHAPE),
+    (dict(D=96), pa.ATTN_ERR_UNSUPPORTED), (dict(D=256), pa.ATTN_ERR_UNSUPPORTED),
+    (dict(dtype=2), pa.ATTN_ERR_UNSUPPORTED),
+    (dict(B=1 << 20, Hq=1 << 10, Hkv=1 << 10, Lq=1 << 20, Lk=1 << 20), pa.ATTN_ERR_SHAPE),
+])
+def test_fwd_rejects_bad_arguments(lib, kw, code):
+    assert fwd(lib, **kw) == code
+
+
+def dec(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=2, Hq=8, Hkv=2, Lk=100, D=128, scale=0.1,
+        slopes=NULL, S=4, ws=FAKE, ws_bytes=1 << 30, dtype=0):
+    return lib.attn_decode(q, k, v, o, B, Hq, Hkv, Lk, D, scale, slopes, S, ws, ws_bytes, dtype, NULL)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=NULL), pa.ATTN_ERR_NULL), (dict(ws=NULL), pa.ATTN_ERR_NULL),
+    (dict(B=0), pa.ATTN_ERR_SHAPE), (dict(Hq=6, Hkv=4), pa.ATTN_ERR_SHAPE),
+    (dict(Lk=0), pa.ATTN_ERR_SHAPE), (dict(S=-1), pa.ATTN_ERR_SHAPE),
+    (dict(scale=float("nan")), pa.ATTN_ERR_SHAPE),
+    (dict(D=32), pa.ATTN_ERR_UNSUPPORTED), (dict(dtype=7), pa.ATTN_ERR_UNSUPPORTED),
+    (dict(ws_bytes=100), pa.ATTN_ERR_WORKSPACE),
+    (dict(ws=ctypes.c_void_p(0x1004)), pa.ATTN_ERR_WORKSPACE),   # not 16-byte aligned
+])
+def test_decode_rejects_bad_arguments(lib, kw, code):
+    assert dec(lib, **kw) == code
+
+
+def test_workspace_size_formula(lib):
+    for B, Hq, D, S in [(1, 1, 64, 1), (8, 32, 128, 32), (16, 32, 128, 64), (3, 5, 64, 7)]:
+        n = B * Hq * S * (D + 2) * 4
+        got = pa.attn_decode_workspace_bytes(B, Hq, D, S)
+        assert got >= n and got - n < 256 and got % 256 == 0
+    assert pa.attn_decode_workspace_bytes(0, 1, 64, 1) == 0
+    assert pa.attn_decode_workspace_bytes(1, 1, 96, 1) == 0
+    assert pa.attn_decode_workspace_bytes(1, 1, 64, 0) == 0
+
+
+def test_workspace_check_uses_resolved_split_count(lib):
+    """With num_splits = 0 the size check uses the heuristic's chunk count."""
+    S = pa.attn_decode_num_splits(2, 8, 2, 100, 128)
+    need = pa.attn_decode_workspace_bytes(2, 8, 128, S)
+    assert dec(lib, S=0, ws_bytes=need - 256) == pa.ATTN_ERR_WORKSPACE
+
+
+def test_num_splits_heuristic(lib):
+    assert pa.attn_decode_num_splits(8, 32, 32, 8192, 128) >= 16
+    assert pa.attn_decode_num_splits(16, 32, 8, 32768, 128) >= 16
+    assert pa.attn_decode_num_splits(1, 1, 1, 1, 64) == 1
+    assert pa.attn_decode_num_splits(1, 1, 1, 300, 64) == 2    # chunks of >= 256 keys
+    assert pa.attn_decode_num_splits(0, 1, 1, 300, 64) == 0
+    for B, Hq, Hkv, Lk in [(1, 4, 2, 777), (4, 16, 16, 5000), (2, 64, 8, 100000)]:
+        S = pa.attn_decode_num_splits(B, Hq, Hkv, Lk, 128)
+        assert 1 <= S <= -(-Lk // 256)
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    q = torch.zeros(1, 1, 4, 64, dtype=torch.float16)
+    with pytest.raises(ValueError):
+        pa.attn_fwd(q, q, q)

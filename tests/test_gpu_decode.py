@@ -1,0 +1,109 @@
+"""GPU parity of split-k decode (attn_decode) against the fp64 oracle.
+
+Besides the final output, the workspace partials written by the split kernel
+(the local nests) are compared element by element with the oracle's own
+local nests, and the result must not depend on the number of chunks.
+"""
+
+import functools
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2510_08726_amd as pa
+from oracle import splitk
+from paper_2510_08726_amd.workloads import WORKLOADS, alibi_slopes, make_inputs, random_tensors
+from gpu_common import assert_close, host32, host64, oracle_fwd, run_fwd
+
+pytestmark = pytest.mark.gpu
+
+
+def run_decode(q, k, v, *, scale, slopes=None, num_splits=0):
+    dev = torch.device("cuda")
+    B, Hq, _, D = q.shape
+    Hkv, Lk = k.shape[1], k.shape[2]
+    S = num_splits or pa.attn_decode_num_splits(B, Hq, Hkv, Lk, D)
+    ws = torch.empty(pa.attn_decode_workspace_bytes(B, Hq, D, S), dtype=torch.uint8, device=dev)
+    o = pa.attn_decode(q.to(dev), k.to(dev), v.to(dev), scale=scale,
+                       alibi_slopes=None if slopes is None else slopes.to(dev),
+                       num_splits=num_splits, workspace=ws)
+    torch.cuda.synchronize()
+    return o, ws, S
+
+
+CASES = [  # B, Hq, Hkv, Lk, D, dtype, S, alibi
+    (2, 8, 2, 1000, 128, "f16", 3, False),
+    (3, 4, 4, 777, 64, "bf16", 5, False),
+    (2, 16, 2, 4096, 128, "f16", 0, False),
+    (1, 6, 2, 333, 128, "bf16", 4, True),      # 3 query heads per KV head
+    (2, 8, 8, 1024, 64, "f16", 1, True),
+    (1, 4, 1, 10, 128, "f16", 6, False),       # chunks of 2 keys, the last chunk empty
+    (1, 2, 2, 1, 64, "f16", 4, False),         # one key, three empty chunks
+    (1, 32, 4, 2500, 128, "bf16", 100, False),
+    (2, 16, 1, 3000, 64, "bf16", 7, True),     # 16 query heads per KV head
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
+def test_decode_matches_oracle(case):
+    B, Hq, Hkv, Lk, D, dt, S, alibi = case
+    print(f"decode case {case}", flush=True)
+    q, k, v = random_tensors([(B, Hq, 1, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], dt, seed=zlib.crc32(repr(case).encode()) % 1000)
+    sl = alibi_slopes(Hq) if alibi else None
+    scale = D ** -0.5
+    o, ws, Sres = run_decode(q, k, v, scale=scale, slopes=sl, num_splits=S)
+    ref = oracle_fwd(q, k, v, scale=scale, causal=True, slopes=sl)
+    assert_close(host32(o), ref, f"decode {case}")
+
+    # the local nests, element by element (natural-log units)
+    o_l, m_l, s_l = [t.cpu().numpy().astype(np.float64) for t in pa.decode_partials(ws, B, Hq, D, Sres)]
+    ro, rm, rs = splitk.split_local(host32(q), host32(k), host32(v), scale=scale, num_splits=Sres,
+                                    causal=True, alibi_slopes=None if sl is None else host64(sl))
+    ro, rm, rs = ro[:, :, 0], rm[:, :, 0], rs[:, :, 0]
+    empty = np.isneginf(rm)
+    assert np.array_equal(np.isneginf(m_l), empty)
+    assert np.all(s_l[empty] == 0) and np.all(o_l[empty] == 0)
+    live = ~empty
+    np.testing.assert_allclose(m_l[live], rm[live], atol=1e-4, rtol=1e-5)
+    np.testing.assert_allclose(s_l[live], rs[live], rtol=2e-4)
+    np.testing.assert_allclose((o_l / np.where(live, s_l, 1)[..., None])[live],
+                               (ro / np.where(live, rs, 1)[..., None])[live], atol=2e-3)
+
+
+def test_decode_independent_of_split_count_and_equals_prefill_row():
+    B, Hq, Hkv, Lk, D = 2, 8, 2, 3000, 128
+    q, k, v = random_tensors([(B, Hq, 1, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], "f16", seed=31)
+    scale = D ** -0.5
+    outs = [host32(run_decode(q, k, v, scale=scale, num_splits=S)[0]) for S in (1, 2, 16, 64, 3000)]
+    single = host32(run_fwd(q, k, v, scale=scale, causal=True))
+    ref = oracle_fwd(q, k, v, scale=scale, causal=True)
+    for o in outs + [single]:
+        assert_close(o, ref, "decode vs oracle")
+    for o in outs[1:] + [single]:
+        assert_close(o, outs[0], "decode(S) vs decode(1)")
+
+
+def test_decode_is_deterministic():
+    q, k, v = random_tensors([(4, 8, 1, 128), (4, 2, 5000, 128), (4, 2, 5000, 128)], "bf16", seed=32)
+    a = run_decode(q, k, v, scale=0.1, num_splits=13)[0]
+    b = run_decode(q, k, v, scale=0.1, num_splits=13)[0]
+    assert torch.equal(a, b)
+
+
+@functools.lru_cache(maxsize=1)
+def _workload_run(name):
+    w = WORKLOADS[name]
+    q, k, v, sl = make_inputs(w)
+    o, ws, S = run_decode(q, k, v, scale=w.sm_scale, slopes=sl, num_splits=w.num_splits)
+    return w, q, k, v, sl, o.cpu()
+
+
+@pytest.mark.parametrize("name", ["mha_decode", "gqa_long_decode"])
+def test_decode_workload_full(name):
+    """Every output row of the full-size decode workloads vs the oracle."""
+    print(f"decode workload {name}", flush=True)
+    w, q, k, v, sl, o = _workload_run(name)
+    ref = oracle_fwd(q, k, v, scale=w.sm_scale, causal=True, slopes=sl)
+    assert_close(host32(o), ref, name)

@@ -1,0 +1,137 @@
+"""GPU parity of the fused prefill kernel (attn_fwd) against the fp64 oracle.
+
+Small shapes span several 128-row query blocks and 64-key tiles with ragged
+tails and are compared element by element; the full-size workloads run in the
+launch configuration the bench times and are compared on sampled rows the
+oracle computes one by one.
+"""
+
+import functools
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2510_08726_amd as pa
+from paper_2510_08726_amd.workloads import WORKLOADS, alibi_slopes, make_inputs, random_tensors
+from gpu_common import assert_close, host32, oracle_fwd, run_fwd
+
+pytestmark = pytest.mark.gpu
+
+CASES = [  # B, Hq, Hkv, Lq, Lk, D, dtype, causal, alibi
+    (1, 2, 2, 128, 128, 64, "f16", False, False),
+    (2, 4, 4, 333, 333, 64, "f16", True, False),
+    (2, 4, 2, 200, 457, 128, "bf16", True, False),
+    (1, 4, 4, 300, 300, 128, "f16", False, False),
+    (2, 8, 2, 257, 257, 128, "bf16", True, True),
+    (1, 2, 2, 190, 64, 64, "f16", True, False),     # Lq > Lk: the first rows see no key
+    (1, 2, 1, 1, 300, 128, "f16", True, False),     # a single query row
+    (1, 3, 1, 65, 65, 64, "bf16", False, True),     # 3 query heads per KV head
+    (1, 4, 4, 130, 70, 128, "f16", False, False),
+    (1, 2, 2, 1, 1, 64, "bf16", True, True),
+    (1, 2, 2, 520, 520, 64, "f16", True, True),
+    (1, 1, 1, 129, 1000, 128, "bf16", False, False),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
+def test_prefill_matches_oracle(case):
+    B, Hq, Hkv, Lq, Lk, D, dt, causal, alibi = case
+    print(f"prefill case {case}", flush=True)
+    q, k, v = random_tensors([(B, Hq, Lq, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], dt, seed=zlib.crc32(repr(case).encode()) % 1000)
+    sl = alibi_slopes(Hq) if alibi else None
+    scale = D ** -0.5
+    o = run_fwd(q, k, v, scale=scale, causal=causal, slopes=sl)
+    ref = oracle_fwd(q, k, v, scale=scale, causal=causal, slopes=sl)
+    assert_close(host32(o), ref, f"prefill {case}")
+    if causal and Lq > Lk:
+        assert torch.all(o[:, :, :Lq - Lk] == 0)
+
+
+@pytest.mark.parametrize("scale,alibi", [(0.0, False), (0.0, True), (-0.2, False), (-0.2, True), (3.0, False)])
+def test_prefill_special_scales(scale, alibi):
+    """scale 0 (uniform / geometric weights), negative scale, large scores."""
+    B, H, L, D = 1, 4, 200, 64
+    q, k, v = random_tensors([(B, H, L, D)] * 3, "f16", seed=21)
+    sl = alibi_slopes(H) if alibi else None
+    o = run_fwd(q, k, v, scale=scale, causal=True, slopes=sl)
+    ref = oracle_fwd(q, k, v, scale=scale, causal=True, slopes=sl)
+    assert_close(host32(o), ref, f"scale={scale} alibi={alibi}")
+
+
+def test_prefill_constant_v():
+    B, H, L, D = 1, 2, 300, 128
+    q, k = random_tensors([(B, H, L, D)] * 2, "f16", seed=22)
+    c = torch.linspace(-3, 3, D, dtype=torch.float16)
+    v = c.expand(B, H, L, D).contiguous()
+    o = run_fwd(q, k, v, scale=D ** -0.5, causal=True)
+    err = (o.float().cpu() - c.float()).abs().max().item()
+    assert err <= 2e-3, err
+
+
+def test_prefill_peak_in_last_tile_selects_its_value_row():
+    """The repair factor must discount every earlier tile once the max jumps."""
+    B, H, L, D = 1, 1, 300, 64
+    q, k, v = random_tensors([(B, H, L, D)] * 3, "f16", seed=23)
+    q = q * 0.05
+    k = k * 0.05
+    jstar = L - 1
+    q[..., 0] = 5.0
+    k[0, 0, jstar, 0] = 6.0          # q.k* = 30 for every row, others < ~0.5
+    q, k = q.contiguous(), k.contiguous()
+    o = run_fwd(q, k, v, scale=1.0, causal=False)
+    np.testing.assert_allclose(host32(o)[0, 0], np.broadcast_to(host32(v)[0, 0, jstar], (L, D)), atol=2e-3)
+
+
+@pytest.mark.parametrize("direction", [1, -1])
+def test_prefill_monotone_scores(direction):
+    """Scores that rise (the max moves at every tile) or fall along the keys."""
+    B, H, L, D = 1, 2, 400, 64
+    _, _, v = random_tensors([(B, H, L, D)] * 3, "bf16", seed=24)
+    u = torch.zeros(D)
+    u[0] = 1.0
+    q = (u * 2.0).expand(B, H, L, D).to(torch.bfloat16).contiguous()
+    ramp = torch.linspace(0, 8, L) * direction
+    k = (ramp[:, None] * u[None, :]).expand(B, H, L, D).to(torch.bfloat16).contiguous()
+    o = run_fwd(q, k, v, scale=1.0, causal=True)
+    ref = oracle_fwd(q, k, v, scale=1.0, causal=True)
+    assert_close(host32(o), ref, f"monotone {direction}")
+
+
+def test_prefill_is_deterministic():
+    w = WORKLOADS["causal_mha_prefill"]
+    q, k, v = random_tensors([(2, 8, 700, 128), (2, 8, 700, 128), (2, 8, 700, 128)], "f16", seed=25)
+    a = run_fwd(q, k, v, scale=w.sm_scale, causal=True)
+    b = run_fwd(q, k, v, scale=w.sm_scale, causal=True)
+    assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads (the bench's launch configuration), sampled rows
+
+@functools.lru_cache(maxsize=1)
+def _workload_run(name):
+    w = WORKLOADS[name]
+    q, k, v, sl = make_inputs(w)
+    o = run_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl)
+    return w, q, k, v, sl, o.cpu()
+
+
+@pytest.mark.parametrize("name", ["tiny_noncausal", "causal_mha_prefill", "gqa_causal_prefill",
+                                  "alibi_causal_prefill"])
+def test_prefill_workload_sampled_rows(name):
+    print(f"prefill workload {name}", flush=True)
+    w, q, k, v, sl, o = _workload_run(name)
+    rng = np.random.Generator(np.random.PCG64(99))
+    L = w.Lq
+    rows = sorted(set([0, 1, 2, 31, 32, 63, 64, 127, 128, 129, L // 2, L - 65, L - 64, L - 2, L - 1]
+                      + list(rng.integers(0, L, 16))))
+    rows = [r for r in rows if 0 <= r < L]
+    heads = sorted(set([(0, 0), (w.B - 1, w.Hq - 1), (0, w.Hq // 2)]
+                       + [(int(rng.integers(w.B)), int(rng.integers(w.Hq))) for _ in range(3)]))
+    ref = oracle_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl, rows=rows, heads=heads)
+    got = host32(o)[:, :, rows]
+    sel_b = [b for b, _ in heads]
+    sel_h = [h for _, h in heads]
+    assert_close(got[sel_b, sel_h], ref[sel_b, sel_h], f"{name} sampled")
