@@ -4,8 +4,7 @@
 // "Privatization" (a local max per key tile, then the running max).
 //
 // Work split.  One workgroup = 8 wave64s = 256 query rows of one (batch,
-// query head).  Each wave owns 32 rows for the whole key loop; the two waves
-// that share a SIMD (waves s and s + 4) own adjacent 32-row blocks.  Key tiles
+// query head).  Each wave owns 32 rows for the whole key loop.  Key tiles
 // are BN = 64 keys.  Per tile j and wave:
 //
 //   S^T = K_j . Q^T            32x32x16 MFMAs, K from LDS, Q resident in VGPRs
@@ -16,27 +15,23 @@
 //                              before the second matmul)
 //   l   = a l + rowsum P       summed from the rounded P with v_dot2, so the
 //                              weights applied to V sum exactly to l
-//   O^T = a O^T + V_j^T . P^T  32x32x16 MFMAs, V^T from LDS, P taken straight
+//   O^T = a O^T + V_j^T . P^T  32x32x16 MFMAs, V from LDS, P taken straight
 //                              from the S^T accumulator registers
 //
 // Computing S transposed puts one query row per lane (rows are the MFMA N
 // index): row reductions stay in registers, the per-row repair of O^T is a
 // per-lane scale, and the fp32 S^T accumulator converts in place into the B
-// operand of the P.V product.  V tiles are stored transposed in LDS (keys
-// contiguous, permuted inside 16-key slices to the order in which the S^T
-// accumulator holds keys), so every MFMA operand is one 16-byte LDS read.
+// operand of the P.V product.  V stays row-major in LDS; its operand is
+// gathered with the gfx950 transposing LDS read, in the key order in which
+// the S^T accumulator holds keys.
 //
-// Ping-pong.  The two waves on a SIMD alternate between an MFMA phase and a
-// VALU phase, one phase apart, separated by workgroup barriers:
-//   MFMA phase of tile j:  S^T of tile j, and the P.V product of tile j-1
-//                          (deferred by one tile), plus staging of the next
-//                          K or V tile (global -> registers -> LDS)
-//   VALU phase of tile j:  softmax of tile j, repair of O^T and l
-// While one wave keeps the matrix core busy the other runs the exponentials,
-// so MFMA and softmax work overlap on every SIMD.  The repair of O^T by tile
-// j's factor always follows the P.V of tile j-1, keeping O^T consistent with
-// the running max.
-//
+// Schedule.  The 8 waves run the tile loop independently between one
+// barrier per tile; the two waves sharing a SIMD (rows 32 s and 32 s + 128)
+// interleave their MFMA and softmax work.  All 512 threads stage K and V of
+// tile j+1 into the other LDS buffer pair while tile j is computed, from
+// registers loaded one tile earlier, so the global loads stay in flight
+// across a whole tile.
+
 // Lazy repair.  The running max used in the exponent is only moved when a
 // row's tile max exceeds it by more than 2^8 (in log2 units); until then the
 // stale max keeps every P <= 2^8 (well inside the fp16 / bf16 range) and the
@@ -56,12 +51,36 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kGroupThreads = 256;          // one ping-pong group = 4 waves, one per SIMD
 constexpr int BM = 32 * kWaves;             // query rows per workgroup
 constexpr int BN = 64;                      // keys per tile
-constexpr int KPAD = 8;                     // elements of padding per K row in LDS
-constexpr int VPAD = 8;                     // elements of padding per V^T row in LDS
 constexpr float kLazyThreshold = 8.f;       // log2 units
+
+// K and V tiles live in LDS row-major, [BN][D], with the 16-byte chunks of
+// each row XOR-swizzled: chunk c of row r sits at chunk position c ^ swz(r).
+// That keeps the three access patterns conflict free: the staging stores
+// (one row per 16 lanes), the K operand reads (16 consecutive rows at one
+// chunk) and the transposing V reads (4 consecutive rows x 4 consecutive
+// chunks per half-wave).
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if (D == 128) return 4 * (r & 3) + ((r >> 2) & 3);
+  return 4 * ((r >> 1) & 1) + ((r >> 2) & 3);
+}
+
+template <int D>
+__device__ __forceinline__ int lds_off(int r, int c) {  // element offset of chunk c of row r
+  return r * D + 8 * (c ^ swz<D>(r));
+}
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+
+// Transposing LDS read: within each 16-lane group, output lane i element j is
+// element (i % 4) of the 8 bytes addressed by lane (i / 4 + 4 j).
+__device__ __forceinline__ uint2 lds_read_tr(const void* p) {
+  v4s r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p));
+  return __builtin_bit_cast(uint2, r);
+}
 
 __device__ __forceinline__ float row_max_across_halves(float x) {
   return fmaxf(x, __shfl_xor(x, 32, 64));
@@ -71,23 +90,13 @@ __device__ __forceinline__ float row_sum_across_halves(float x) {
   return x + __shfl_xor(x, 32, 64);
 }
 
-// Column, inside a V^T row, at which the 4-key group q4 (keys 4 q4 .. 4 q4 + 3)
-// is stored: within each 16-key slice, key offset 8a + 4h + i goes to
-// 8h + 4a + i, so that lane half h finds its 8 keys in one 16-byte chunk.
-__device__ __forceinline__ int vt_col(int q4) {
-  return 4 * ((q4 & ~3) | ((q4 & 1) << 1) | ((q4 >> 1) & 1));
-}
-
 template <int D, typename T, bool CAUSAL, bool ALIBI>
 struct Prefill {
   typedef Elem<T> E;
   typedef typename E::vec8 vec8;
   static constexpr int KX = D / 16;                        // MFMA K-steps of Q.K^T
   static constexpr int DB = D / 32;                        // 32-dim blocks of O^T
-  static constexpr int KS = BN * (D + KPAD);               // K tile: [BN][D + KPAD]
-  static constexpr int VS = D * (BN + VPAD);               // V^T tile: [D][BN + VPAD]
-  static constexpr int KCH = BN * D / 8 / kGroupThreads;   // 16-byte K chunks per group thread
-  static constexpr int VBL = (BN / 4) * (D / 4) / kGroupThreads;  // 4x4 V blocks per group thread
+  static constexpr int TE = BN * D;                        // elements of one K or V tile
 
   struct State {
     float m;          // reference max (log2 units of the exponent)
@@ -95,30 +104,40 @@ struct Prefill {
     f32x16 o[DB];     // O^T accumulators
   };
 
-  // S^T = K tile . Q^T: s[kb] covers keys 32 kb .. 32 kb + 31.
+  // S^T = K tile . Q^T: s[kb] covers keys 32 kb .. 32 kb + 31.  A operand:
+  // lane (n, hh) reads row 32 kb + n, head dims 16 kx + 8 hh .. + 7.
   static __device__ __forceinline__ void qk(f32x16 (&s)[2], const T* ks, const vec8 (&qf)[KX], int n, int hh) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
 #pragma unroll
-      for (int kx = 0; kx < KX; ++kx) {
-        const uint4 a = *reinterpret_cast<const uint4*>(ks + (32 * kb + n) * (D + KPAD) + 16 * kx + 8 * hh);
+    for (int kx = 0; kx < KX; ++kx)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {   // the two accumulator chains alternate
+        const uint4 a = *reinterpret_cast<const uint4*>(ks + lds_off<D>(32 * kb + n, 2 * kx + hh));
         s[kb] = E::mfma(__builtin_bit_cast(vec8, a), qf[kx], s[kb]);
       }
-    }
   }
 
-  // O^T += V^T P^T; A operand: lane (n, hh) reads V^T[32 db + n][16 c16 + 8 hh .. + 7].
-  static __device__ __forceinline__ void pv(State& st, const uint32_t (&pw)[BN / 16][4], const T* vs, int n,
-                                            int hh) {
+  // O^T += V^T P^T.  The A operand (head dims 32 db + m, 16-key slice c16) is
+  // gathered from the row-major V tile with two transposing reads: lane
+  // (m, half hh) receives keys 16 c16 + 4 hh + 0..3 and 16 c16 + 8 + 4 hh + 0..3,
+  // the order in which the S^T accumulator holds keys in the B operand.
+  static __device__ __forceinline__ void pv(State& st, const uint32_t (&pw)[BN / 16][4], const T* vs, int lane) {
+    const int G = lane >> 4, i = lane & 15;
+    const int hh = G >> 1;
 #pragma unroll
     for (int c16 = 0; c16 < BN / 16; ++c16) {
       const vec8 bop = __builtin_bit_cast(vec8, make_uint4(pw[c16][0], pw[c16][1], pw[c16][2], pw[c16][3]));
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const uint4 a = *reinterpret_cast<const uint4*>(vs + (32 * db + n) * (BN + VPAD) + 16 * c16 + 8 * hh);
-        st.o[db] = E::mfma(__builtin_bit_cast(vec8, a), bop, st.o[db]);
+        const int d = 32 * db + 16 * (G & 1) + 4 * (i & 3);   // this source lane's 4 head dims
+        const int k = 16 * c16 + 4 * hh + (i >> 2);            // this source lane's key
+        const uint2 lo = lds_read_tr(vs + lds_off<D>(k, d >> 3) + (d & 7));
+        const uint2 hi = lds_read_tr(vs + lds_off<D>(k + 8, d >> 3) + (d & 7));
+        const vec8 a = __builtin_bit_cast(vec8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        st.o[db] = E::mfma(a, bop, st.o[db]);
       }
     }
   }
@@ -186,17 +205,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   typedef typename PF::vec8 vec8;
   typedef typename PF::State State;
   constexpr int KX = PF::KX;
-  constexpr int KS = PF::KS, VS = PF::VS;
-  constexpr int KCH = PF::KCH, VBL = PF::VBL;
-  // [K buf 0][K buf 1][V^T buf 0][V^T buf 1]
-  __shared__ __attribute__((aligned(16))) T smem[2 * KS + 2 * VS];
+  constexpr int TE = PF::TE;
+  constexpr int CH = BN * D / 8 / kThreads;   // 16-byte chunks of one tile per thread
+  // [K buf 0][K buf 1][V buf 0][V buf 1]
+  __shared__ __attribute__((aligned(16))) T smem[4 * TE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int grp = wave >> 2;        // 0: first MFMA phase at phase 0; 1: one phase later
-  const int simd = wave & 3;
-  const int gt = tid & (kGroupThreads - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31;
   const int hh = lane >> 5;
 
@@ -212,8 +228,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   const int Lq = p.Lq, Lk = p.Lk;
   const int off = Lk - Lq;
   const int i0 = qb * BM;
-  const int iw = i0 + 64 * simd + 32 * grp;   // first row of this wave
-  const int row = iw + n;                      // this lane's row
+  const int iw = i0 + 32 * wave;   // first row of this wave
+  const int row = iw + n;          // this lane's row
 
   // Tiles: the workgroup stages [0, n_wg); this wave computes [0, n_w); tiles
   // [0, fm_w) need no mask for any of its rows.
@@ -244,71 +260,32 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   }
 
   T* const kbuf = smem;
-  T* const vbuf = smem + 2 * KS;
+  T* const vbuf = smem + 2 * TE;
 
-  // Staging.  Group 0 stages K tiles, group 1 stages V tiles (transposed),
-  // each through registers loaded one tile ahead.
-  uint4 kreg[KCH];
-  uint2 vreg[VBL][4];
-  auto kload = [&](int t) {
+  // Staging of K and V tiles through registers, one tile ahead: thread t owns
+  // chunks idx = c * 512 + t (row idx / (D/8), chunk idx % (D/8)), so 16
+  // lanes read one row.  Rows past Lk read row Lk - 1 instead: such keys are
+  // always masked, so their K values never count and their V rows meet P = 0.
+  u32x4 kst[CH], vst[CH];
+  auto sload = [&](int t) {
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      const int idx = c * kGroupThreads + gt;
-      const int key = idx / (D / 8), ch = idx % (D / 8);
-      const int g = t * BN + key;
-      kreg[c] = (t < n_wg && g < Lk) ? *reinterpret_cast<const uint4*>(kp + (size_t)g * D + ch * 8)
-                                     : make_uint4(0, 0, 0, 0);
+    for (int c = 0; c < CH; ++c) {
+      const int idx = c * kThreads + tid;
+      const int r = idx / (D / 8), ch = idx % (D / 8);
+      const size_t g = (size_t)min(t * BN + r, Lk - 1) * D + ch * 8;
+      kst[c] = *reinterpret_cast<const u32x4*>(kp + g);
+      vst[c] = *reinterpret_cast<const u32x4*>(vp + g);
     }
   };
-  auto kstore = [&](int t) {
-    T* ks = kbuf + (t & 1) * KS;
+  auto sstore = [&](int t) {
+    T* kd = kbuf + (t & 1) * TE;
+    T* vd = vbuf + (t & 1) * TE;
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) {
-      const int idx = c * kGroupThreads + gt;
-      const int key = idx / (D / 8), ch = idx % (D / 8);
-      *reinterpret_cast<uint4*>(ks + key * (D + KPAD) + ch * 8) = kreg[c];
-    }
-  };
-  // V block idx -> (kq, dq): 16 consecutive lanes take 16 key groups of one
-  // dim group; the two half-waves take dim groups two apart, so the 8-byte
-  // stores of a half-wave cover all 64 LDS banks once.
-  auto vblock = [&](int bl, int& kq, int& dq) {
-    const int idx = bl * kGroupThreads + gt;
-    kq = idx & 15;
-    const int dl = idx >> 4;
-    dq = (dl & ~3) | ((dl & 1) << 1) | ((dl >> 1) & 1);
-  };
-  auto vload = [&](int t) {
-#pragma unroll
-    for (int bl = 0; bl < VBL; ++bl) {
-      int kq, dq;
-      vblock(bl, kq, dq);
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int g = t * BN + 4 * kq + kk;
-        vreg[bl][kk] = (t < n_wg && g < Lk) ? *reinterpret_cast<const uint2*>(vp + (size_t)g * D + 4 * dq)
-                                            : make_uint2(0, 0);
-      }
-    }
-  };
-  auto vstore = [&](int t) {
-    T* vs = vbuf + (t & 1) * VS;
-#pragma unroll
-    for (int bl = 0; bl < VBL; ++bl) {
-      int kq, dq;
-      vblock(bl, kq, dq);
-      const uint2* r = vreg[bl];
-      // 4 keys x 4 dims of 16-bit values, transposed to 4 dims x 4 keys.
-      uint2 t0, t1, t2, t3;
-      t0.x = (r[0].x & 0xffffu) | (r[1].x << 16);        t0.y = (r[2].x & 0xffffu) | (r[3].x << 16);
-      t1.x = (r[0].x >> 16) | (r[1].x & 0xffff0000u);    t1.y = (r[2].x >> 16) | (r[3].x & 0xffff0000u);
-      t2.x = (r[0].y & 0xffffu) | (r[1].y << 16);        t2.y = (r[2].y & 0xffffu) | (r[3].y << 16);
-      t3.x = (r[0].y >> 16) | (r[1].y & 0xffff0000u);    t3.y = (r[2].y >> 16) | (r[3].y & 0xffff0000u);
-      T* dst = vs + (4 * dq) * (BN + VPAD) + vt_col(kq);
-      *reinterpret_cast<uint2*>(dst) = t0;
-      *reinterpret_cast<uint2*>(dst + (BN + VPAD)) = t1;
-      *reinterpret_cast<uint2*>(dst + 2 * (BN + VPAD)) = t2;
-      *reinterpret_cast<uint2*>(dst + 3 * (BN + VPAD)) = t3;
+    for (int c = 0; c < CH; ++c) {
+      const int idx = c * kThreads + tid;
+      const int r = idx / (D / 8), ch = idx % (D / 8);
+      *reinterpret_cast<u32x4*>(kd + lds_off<D>(r, ch)) = kst[c];
+      *reinterpret_cast<u32x4*>(vd + lds_off<D>(r, ch)) = vst[c];
     }
   };
 
@@ -324,57 +301,40 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   float sl2 = 0.f;
   if (ALIBI) sl2 = p.slopes[hq] * kLog2e;
 
-  // Prologue: K_0 into LDS (all threads share the chunks), then group 0 holds
-  // K_1 in registers and group 1 holds V_0.
-  if (grp == 0) {
-    kload(0);
-    kstore(0);
-    kload(1);
-  } else {
-    vload(0);
-  }
-  __syncthreads();
-
   f32x16 s[2];
   uint32_t pw[BN / 16][4];
 
-  // Phase ph: group g runs the MFMA phase of tile (ph - g) / 2 when ph - g is
-  // even and the VALU phase of tile (ph - g - 1) / 2 when it is odd.
-  const int nphases = 2 * n_wg + 2;
-  for (int ph = 0; ph < nphases; ++ph) {
-    const int u = ph - grp;
-    if (u >= 0 && (u & 1) == 0) {
-      const int j = u >> 1;
-      // MFMA phase of tile j: P.V of tile j-1 (its P is ready), S^T of tile j.
-      if (j >= 1 && j <= n_w) PF::pv(st, pw, vbuf + ((j - 1) & 1) * VS, n, hh);
-      if (j < n_w) PF::qk(s, kbuf + (j & 1) * KS, qf, n, hh);
-      // staging: group 0 writes K_{j+1} and loads K_{j+2}; group 1 writes V_j and loads V_{j+1}
-      if (grp == 0) {
-        if (j + 1 < n_wg) kstore(j + 1);
-        kload(j + 2);
-      } else {
-        if (j < n_wg) vstore(j);
-        vload(j + 1);
-      }
-    } else if (u >= 1) {
-      const int j = (u - 1) >> 1;
-      // VALU phase of tile j.
-      if (j < n_w) {
-        float alpha = 1.f;
-        bool moved;
-        if (j < fm_w)
-          moved = PF::template softmax<false>(st, s, pw, alpha, c, sl2, j * BN, row, off, Lk, hh);
-        else
-          moved = PF::template softmax<true>(st, s, pw, alpha, c, sl2, j * BN, row, off, Lk, hh);
-        if (moved) {
+  if (n_wg > 0) {
+    sload(0);
+    sstore(0);
+    sload(1);
+  }
+  __syncthreads();
+
+  for (int j = 0; j < n_wg; ++j) {
+    const T* kc = kbuf + (j & 1) * TE;
+    const T* vc = vbuf + (j & 1) * TE;
+    if (j < n_w) {
+      PF::qk(s, kc, qf, n, hh);
+      float alpha = 1.f;
+      bool moved;
+      if (j < fm_w)
+        moved = PF::template softmax<false>(st, s, pw, alpha, c, sl2, j * BN, row, off, Lk, hh);
+      else
+        moved = PF::template softmax<true>(st, s, pw, alpha, c, sl2, j * BN, row, off, Lk, hh);
+      if (moved) {
 #pragma unroll
-          for (int db = 0; db < PF::DB; ++db)
+        for (int db = 0; db < PF::DB; ++db)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) st.o[db][r] *= alpha;
-        }
+          for (int r = 0; r < 16; ++r) st.o[db][r] *= alpha;
       }
+      PF::pv(st, pw, vc, lane);
     }
-    __syncthreads();
+    // Tile j+1 goes into the buffers last read in step j-1; then the loads of
+    // tile j+2 are issued and stay in flight across the barrier.
+    if (j + 1 < n_wg) sstore(j + 1);
+    sload(j + 2);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   }
 
   // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
