@@ -42,6 +42,8 @@
 // Scores are in log2 units: t = s * scale * log2(e) (+ ALiBi bias * log2(e)),
 // so each exponential is one v_exp_f32.
 
+#include <type_traits>
+
 #include "kernel_common.h"
 #include "launch.h"
 
@@ -118,6 +120,15 @@ struct Prefill {
         const uint4 a = *reinterpret_cast<const uint4*>(ks + lds_off<D>(32 * kb + n, 2 * kx + hh));
         s[kb] = E::mfma(__builtin_bit_cast(vec8, a), qf[kx], s[kb]);
       }
+    // Keep kPre K fragments in flight ahead of the MFMA that consumes them.
+    constexpr int kPre = 6;
+    __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
+#pragma unroll
+    for (int g = 0; g < 2 * KX - kPre; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
   }
 
   // O^T += V^T P^T.  The A operand (head dims 32 db + m, 16-key slice c16) is
@@ -140,6 +151,15 @@ struct Prefill {
         st.o[db] = E::mfma(a, bop, st.o[db]);
       }
     }
+    // Keep four operands (eight transposing reads) in flight ahead of the MFMAs.
+    constexpr int kPre = 4;
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPre, 0);
+#pragma unroll
+    for (int g = 0; g < DB * (BN / 16) - kPre; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
   }
 
   // Softmax of one tile: rolling update of the reference max and l, P packed
@@ -264,28 +284,37 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 
   // Staging of K and V tiles through registers, one tile ahead: thread t owns
   // chunks idx = c * 512 + t (row idx / (D/8), chunk idx % (D/8)), so 16
-  // lanes read one row.  Rows past Lk read row Lk - 1 instead: such keys are
-  // always masked, so their K values never count and their V rows meet P = 0.
+  // lanes read one 256-byte row.  Loads go through buffer resources bounded
+  // at the head's Lk rows: rows past Lk read as zero (such keys are always
+  // masked), and the per-lane offsets are loop invariant.
+  const __amdgpu_buffer_rsrc_t krs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(kp), (short)0, Lk * D * (int)sizeof(T), 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(vp), (short)0, Lk * D * (int)sizeof(T), 0x00020000);
+  int goff[CH], loff[CH];
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int idx = c * kThreads + tid;
+    const int r = idx / (D / 8), ch = idx % (D / 8);
+    goff[c] = (r * D + ch * 8) * (int)sizeof(T);
+    loff[c] = lds_off<D>(r, ch);
+  }
   u32x4 kst[CH], vst[CH];
   auto sload = [&](int t) {
+    const int soff = t * BN * D * (int)sizeof(T);
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      const int idx = c * kThreads + tid;
-      const int r = idx / (D / 8), ch = idx % (D / 8);
-      const size_t g = (size_t)min(t * BN + r, Lk - 1) * D + ch * 8;
-      kst[c] = *reinterpret_cast<const u32x4*>(kp + g);
-      vst[c] = *reinterpret_cast<const u32x4*>(vp + g);
+      kst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(krs, goff[c], soff, 0));
+      vst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vrs, goff[c], soff, 0));
     }
   };
-  auto sstore = [&](int t) {
-    T* kd = kbuf + (t & 1) * TE;
-    T* vd = vbuf + (t & 1) * TE;
+  auto sstore = [&](int par) {
+    T* kd = kbuf + par * TE;
+    T* vd = vbuf + par * TE;
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      const int idx = c * kThreads + tid;
-      const int r = idx / (D / 8), ch = idx % (D / 8);
-      *reinterpret_cast<u32x4*>(kd + lds_off<D>(r, ch)) = kst[c];
-      *reinterpret_cast<u32x4*>(vd + lds_off<D>(r, ch)) = vst[c];
+      *reinterpret_cast<u32x4*>(kd + loff[c]) = kst[c];
+      *reinterpret_cast<u32x4*>(vd + loff[c]) = vst[c];
     }
   };
 
@@ -311,9 +340,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   }
   __syncthreads();
 
-  for (int j = 0; j < n_wg; ++j) {
-    const T* kc = kbuf + (j & 1) * TE;
-    const T* vc = vbuf + (j & 1) * TE;
+  // Tile j lives in LDS buffer pair j & 1; the loop is unrolled by two so the
+  // buffer offsets are compile-time constants.
+  auto step = [&](int j, auto parity) {
+    constexpr int par = decltype(parity)::value;
+    const T* kc = kbuf + par * TE;
+    const T* vc = vbuf + par * TE;
     if (j < n_w) {
       PF::qk(s, kc, qf, n, hh);
       float alpha = 1.f;
@@ -330,12 +362,18 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       }
       PF::pv(st, pw, vc, lane);
     }
-    // Tile j+1 goes into the buffers last read in step j-1; then the loads of
-    // tile j+2 are issued and stay in flight across the barrier.
-    if (j + 1 < n_wg) sstore(j + 1);
+    // Tile j+1 goes into the other buffer pair (last read in step j-1); then
+    // the loads of tile j+2 are issued and stay in flight across the barrier.
+    if (j + 1 < n_wg) sstore(par ^ 1);
     sload(j + 2);
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  };
+  int j = 0;
+  for (; j + 1 < n_wg; j += 2) {
+    step(j, std::integral_constant<int, 0>{});
+    step(j + 1, std::integral_constant<int, 1>{});
   }
+  if (j < n_wg) step(j, std::integral_constant<int, 0>{});
 
   // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
   // head dims 32 db + 8 g + 4 hh + 0..3 of its row.
