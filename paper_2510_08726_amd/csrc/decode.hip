@@ -209,30 +209,64 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
   }
 }
 
-// Global nests: one workgroup per (batch, query head), one thread per head dim.
+// Global nests: one workgroup per (batch, query head), one thread per head
+// dim.  Pass 1 takes max_g over all chunk maxima (a block reduction); pass 2
+// computes each chunk's weight exp(max_l - max_g) once into LDS, in batches,
+// and sums the weighted partial outputs and sums with all loads in flight.
+// The workspace is only read.
 template <int D, typename T>
 __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams p) {
-  typedef Elem<T> E;
+  constexpr int kBatch = 512;
+  __shared__ float sh_w[kBatch];
+  __shared__ float sh_l[kBatch];
+  __shared__ float sh_red[D / 64];
   const int row = blockIdx.x;   // b * Hq + hq
   const int d = threadIdx.x;
   const int S = p.splits;
   const float* mp = p.ws_m + (size_t)row * S;
   const float* lp = p.ws_l + (size_t)row * S;
   const float* op = p.ws_o + (size_t)row * S * D + d;
+
+  float mloc = kNegInf;
+  for (int s = d; s < S; s += D) mloc = fmaxf(mloc, mp[s]);
+#pragma unroll
+  for (int x = 32; x >= 1; x >>= 1) mloc = fmaxf(mloc, __shfl_xor(mloc, x, 64));
+  if ((d & 63) == 0) sh_red[d >> 6] = mloc;
+  __syncthreads();
   float M = kNegInf;
-  for (int s = 0; s < S; ++s) M = fmaxf(M, mp[s]);
-  float L = 0.f, acc = 0.f;
+#pragma unroll
+  for (int w = 0; w < D / 64; ++w) M = fmaxf(M, sh_red[w]);
+
+  float acc = 0.f, L = 0.f;
   if (M != kNegInf) {
-    for (int s = 0; s < S; ++s) {
-      const float ms = mp[s];
-      const float w = ms == kNegInf ? 0.f : fast_exp2((ms - M) * kLog2e);
-      L = __builtin_fmaf(w, lp[s], L);
-      acc = __builtin_fmaf(w, op[(size_t)s * D], acc);
+    for (int s0 = 0; s0 < S; s0 += kBatch) {
+      const int ns = min(kBatch, S - s0);
+      for (int s = d; s < ns; s += D) {
+        const float m = mp[s0 + s];
+        sh_w[s] = (m == kNegInf) ? 0.f : fast_exp2((m - M) * kLog2e);
+        sh_l[s] = lp[s0 + s];
+      }
+      __syncthreads();
+      int s = 0;
+      for (; s + 8 <= ns; s += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = op[(size_t)(s0 + s + u) * D];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          acc = __builtin_fmaf(sh_w[s + u], v[u], acc);
+          L = __builtin_fmaf(sh_w[s + u], sh_l[s + u], L);
+        }
+      }
+      for (; s < ns; ++s) {
+        acc = __builtin_fmaf(sh_w[s], op[(size_t)(s0 + s) * D], acc);
+        L = __builtin_fmaf(sh_w[s], sh_l[s], L);
+      }
+      __syncthreads();
     }
   }
   const float out = L > 0.f ? acc / L : 0.f;
-  T* dst = reinterpret_cast<T*>(p.o) + (size_t)row * D + d;
-  *dst = (T)out;
+  reinterpret_cast<T*>(p.o)[(size_t)row * D + d] = (T)out;
 }
 
 template <int D, typename T, int GH>
