@@ -300,12 +300,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     loff[c] = lds_off<D>(r, ch);
   }
   u32x4 kst[CH], vst[CH];
+  // The tile offset is folded into the per-lane (VGPR) offset, which the
+  // buffer range check covers, so rows at or past Lk read as zero.
   auto sload = [&](int t) {
-    const int soff = t * BN * D * (int)sizeof(T);
+    const unsigned tk = (unsigned)t * (unsigned)(BN * D * sizeof(T));
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      kst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(krs, goff[c], soff, 0));
-      vst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vrs, goff[c], soff, 0));
+      kst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(krs, (int)(tk + goff[c]), 0, 0));
+      vst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vrs, (int)(tk + goff[c]), 0, 0));
     }
   };
   auto sstore = [&](int par) {
