@@ -13,8 +13,7 @@
 //   P   = exp2(S - m')         rounded to the input type (the compute
 //                              definition casts exp to the input dtype
 //                              before the second matmul)
-//   l   = a l + rowsum P       summed from the rounded P with v_dot2, so the
-//                              weights applied to V sum exactly to l
+//   l   = a l + rowsum P       fp32 sum of the weights before rounding
 //   O^T = a O^T + V_j^T . P^T  32x32x16 MFMAs, V from LDS, P taken straight
 //                              from the S^T accumulator registers
 //
@@ -198,8 +197,10 @@ struct Prefill {
     st.m = mref;
     alpha = a;
     const float mc = (mref == kNegInf) ? 0.f : mref * ce;
-    const uint32_t ones = E::pack2(1.f, 1.f);
-    float lsum = 0.f;
+    // The row sum adds the fp32 weights (two partial sums); the packed dot
+    // product would sum the rounded weights exactly, but it blocks the MFMA
+    // pipe for far longer than plain adds on gfx950.
+    float lsum0 = 0.f, lsum1 = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -210,10 +211,11 @@ struct Prefill {
           p0 = s[kb][r] == kNegInf ? 0.f : p0;
           p1 = s[kb][r + 1] == kNegInf ? 0.f : p1;
         }
-        const uint32_t w = E::pack2(p0, p1);
-        lsum = E::dot2(w, ones, lsum);
-        pw[2 * kb + r / 8][(r % 8) / 2] = w;
+        lsum0 += p0;
+        lsum1 += p1;
+        pw[2 * kb + r / 8][(r % 8) / 2] = E::pack2(p0, p1);
       }
+    const float lsum = lsum0 + lsum1;
     st.l = __builtin_fmaf(st.l, a, lsum);
     return move;
   }
