@@ -18,10 +18,27 @@ LIB = os.path.join(PKG, "libattn.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
-COMMON = ["-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC]
+COMMON = ["-O3", "-std=c++20", "-fPIC", "-I", INCLUDE, "-I", CSRC]
 DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-command-line-argument"]
-SOURCES = ["prefill.hip", "decode.hip", "attn_api.cpp"]
+# (object name, source, extra flags).  prefill.hip is compiled once per
+# (head dim, element type) shard so its instantiations build in parallel.
+# Its softmax never needs IEEE NaN handling of max: without it, fmaxf of
+# values produced by inline assembly compiles to a plain v_max instead of
+# canonicalising both inputs first.  The prefill device assembly is kept
+# (-save-temps) for the ISA hazard check in the tests.
+UNITS = [(f"prefill{k}", "prefill.hip", ["-fno-honor-nans", f"-DATTN_PREFILL_SHARD={k}", "-save-temps"])
+         for k in range(4)] + [("decode", "decode.hip", []), ("attn_api", "attn_api.cpp", [])]
+
+
+def unit_dir(name):
+    """Working directory of one compile (holds its -save-temps files)."""
+    return os.path.join(OBJDIR, name)
+
+
+def prefill_asm_files():
+    """Device assembly of the prefill shards written by the last build()."""
+    return [os.path.join(unit_dir(f"prefill{k}"), f"prefill-hip-amdgcn-amd-amdhsa-{ARCH}.s") for k in range(4)]
 
 
 def build(verbose=False):
@@ -29,15 +46,17 @@ def build(verbose=False):
     os.makedirs(OBJDIR, exist_ok=True)
     procs = []
     objs = []
-    for src in SOURCES:
+    for name, src, flags in UNITS:
         path = os.path.join(CSRC, src)
-        obj = os.path.join(OBJDIR, src + ".o")
+        obj = os.path.join(OBJDIR, name + ".o")
         objs.append(obj)
-        extra = DEVICE if src.endswith(".hip") else []
+        extra = (DEVICE if src.endswith(".hip") else []) + flags
         cmd = [HIPCC, *COMMON, *extra, "-c", path, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
-        procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
+        os.makedirs(unit_dir(name), exist_ok=True)
+        procs.append((name, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True,
+                                             cwd=unit_dir(name))))
     failed = []
     for src, pr in procs:
         out, _ = pr.communicate()

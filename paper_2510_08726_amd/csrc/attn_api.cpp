@@ -86,7 +86,10 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
     p.c = scale * kLog2e;
     p.qsign = 0;
   } else {
-    p.c = std::fabs(scale) * kLog2e;
+    // Kept above zero so that masked (-inf) scores times c stay -inf when
+    // scale is 0; exp2(s * 1e-30) rounds to exactly 1 for any finite score,
+    // the same weights as c = 0.
+    p.c = std::fmax(std::fabs(scale) * kLog2e, 1e-30f);
     p.qsign = std::signbit(scale) ? 0x80008000u : 0u;
   }
   p.nqb = (int)nqb;

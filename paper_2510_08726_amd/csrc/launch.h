@@ -19,7 +19,8 @@ struct PrefillParams {
   float c;              // |scale| * log2(e) without ALiBi, scale * log2(e) with it
   unsigned qsign;       // 0x80008000 to negate Q (negative scale without ALiBi), else 0
   int nqb;              // query blocks per head
-  int xcd_remap;        // set by the launcher
+  int nheads;           // B * Hq, set by the launcher
+  int nitems;           // nqb * nheads, set by the launcher
 };
 
 struct DecodeParams {
@@ -41,6 +42,11 @@ struct DecodeParams {
 
 int prefill_block_rows();
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
+// One per (head dim, element type); launch_prefill dispatches to them.
+hipError_t launch_prefill_d128_f16(const PrefillParams& p, hipStream_t stream);
+hipError_t launch_prefill_d128_bf16(const PrefillParams& p, hipStream_t stream);
+hipError_t launch_prefill_d64_f16(const PrefillParams& p, hipStream_t stream);
+hipError_t launch_prefill_d64_bf16(const PrefillParams& p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
 
 }  // namespace attn

@@ -3,12 +3,13 @@
 // the plain attention definition, with the tile structure of the appendix
 // "Privatization" (a local max per key tile, then the running max).
 //
-// Work split.  One workgroup = 8 wave64s = 256 query rows of one (batch,
-// query head).  Each wave owns 32 rows for the whole key loop.  Key tiles
-// are BN = 64 keys.  Per tile j and wave:
+// Work split.  One workgroup = 4 wave64s = 256 query rows of one (batch,
+// query head); each wave owns 64 rows (two 32-row blocks) for the whole key
+// loop and runs alone on its SIMD with the full register file.  Key tiles
+// are BN = 32 keys.  Per tile j and wave:
 //
-//   S^T = K_j . Q^T            32x32x16 MFMAs, K from LDS, Q resident in VGPRs
-//   m'  = max(m, rowmax S)     in-lane max + one exchange with lane ^ 32
+//   S^T = K_j . Q^T            32x32x16 MFMAs, K from LDS, Q resident in AGPRs
+//   m'  = max(m, rowmax S)     in-lane max + permlane32 swaps
 //   a   = exp2(m - m')         the repair factor h(t, r, r') = t exp(r - r')
 //   P   = exp2(S - m')         rounded to the input type (the compute
 //                              definition casts exp to the input dtype
@@ -22,15 +23,28 @@
 // per-lane scale, and the fp32 S^T accumulator converts in place into the B
 // operand of the P.V product.  V stays row-major in LDS; its operand is
 // gathered with the gfx950 transposing LDS read, in the key order in which
-// the S^T accumulator holds keys.
+// the S^T accumulator holds keys.  Each K or V operand fragment read from
+// LDS feeds the MFMAs of both 32-row blocks, which halves the LDS traffic
+// per flop compared with 32 rows per wave.
 //
-// Schedule.  The 8 waves run the tile loop independently between one
-// barrier per tile; the two waves sharing a SIMD (rows 32 s and 32 s + 128)
-// interleave their MFMA and softmax work.  All 512 threads stage K and V of
-// tile j+1 into the other LDS buffer pair while tile j is computed, from
-// registers loaded one tile earlier, so the global loads stay in flight
-// across a whole tile.
-
+// Schedule.  On gfx950 a wave's VALU instructions issued behind its own
+// MFMA overlap with it, while VALU work of another wave on the same SIMD
+// barely does.  So every wave software-pipelines its own loop: iteration j
+// issues the MFMAs of S^T for tile j+1 and of P.V for tile j-1, and spreads
+// the softmax of tile j (pure VALU, independent of both) over the gaps
+// between them: the iteration is a fixed sequence of MFMA slots, each
+// followed by its share of the softmax and by the LDS reads of the operands
+// a few fragments ahead, fenced so the compiler keeps that order.  K and V
+// tiles are copied HBM -> LDS by the buffer unit (loads with the LDS bit, no
+// registers involved) into double buffers, one tile ahead of their first
+// use; one barrier per iteration publishes them.
+//
+// The MFMAs are written as inline assembly to fix their register files: the
+// S^T accumulators in VGPRs (the softmax reads them), O^T and Q in AGPRs.
+// The compiler does not model the latency of those instructions, so every
+// VALU reader of an MFMA result is at least two MFMAs and a barrier away
+// from it, or behind explicit s_nop padding.
+//
 // Lazy repair.  The running max used in the exponent is only moved when a
 // row's tile max exceeds it by more than 2^8 (in log2 units); until then the
 // stale max keeps every P <= 2^8 (well inside the fp16 / bf16 range) and the
@@ -41,7 +55,10 @@
 // Scores are in log2 units: t = s * scale * log2(e) (+ ALiBi bias * log2(e)),
 // so each exponential is one v_exp_f32.
 
+#include <algorithm>
+#include <atomic>
 #include <type_traits>
+#include <utility>
 
 #include "kernel_common.h"
 #include "launch.h"
@@ -50,31 +67,38 @@ namespace attn {
 
 namespace {
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int BM = 32 * kWaves;             // query rows per workgroup
-constexpr int BN = 64;                      // keys per tile
+constexpr int RB = 2;                       // 32-row blocks per wave
+constexpr int BMW = 32 * RB;                // query rows per wave
+static_assert(RB == 2, "the row-max exchange and the finalisation handle two row blocks");
+constexpr int BM = BMW * kWaves;            // query rows per workgroup
+constexpr int BN = 32;                      // keys per tile
+constexpr int PFD = 3;                      // operand fragments read ahead
+constexpr int kRing = 4;                    // LDS slots per operand; copies run kRing - 1 tiles ahead
 constexpr float kLazyThreshold = 8.f;       // log2 units
+// Reference max (times c) before the first visible key: finite, so the first
+// tile's decision and repair factor need no special case (its repair factor
+// underflows to 0, and O^T and l are still 0 then).
+constexpr float kMcInit = -1e30f;
+constexpr float kMcFresh = -1e29f;
 
 // K and V tiles live in LDS row-major, [BN][D], with the 16-byte chunks of
 // each row XOR-swizzled: chunk c of row r sits at chunk position c ^ swz(r).
-// That keeps the three access patterns conflict free: the staging stores
-// (one row per 16 lanes), the K operand reads (16 consecutive rows at one
-// chunk) and the transposing V reads (4 consecutive rows x 4 consecutive
-// chunks per half-wave).
+// That keeps the K operand reads (16 consecutive rows at one chunk) and the
+// transposing V reads (4 consecutive rows x 4 consecutive chunks per
+// half-wave) free of bank conflicts; the copy engine writes whole 1 KB
+// blocks, so the swizzle is applied on the global side of the copy.
+// swz depends on r % 16 only.
 template <int D>
 __device__ __forceinline__ int swz(int r) {
   if (D == 128) return 4 * (r & 3) + ((r >> 2) & 3);
   return 4 * ((r >> 1) & 1) + ((r >> 2) & 3);
 }
 
-template <int D>
-__device__ __forceinline__ int lds_off(int r, int c) {  // element offset of chunk c of row r
-  return r * D + 8 * (c ^ swz<D>(r));
-}
-
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
+typedef __attribute__((address_space(3))) void lds_void;
 
 // Transposing LDS read: within each 16-lane group, output lane i element j is
 // element (i % 4) of the 8 bytes addressed by lane (i / 4 + 4 j).
@@ -83,141 +107,415 @@ __device__ __forceinline__ uint2 lds_read_tr(const void* p) {
   return __builtin_bit_cast(uint2, r);
 }
 
-__device__ __forceinline__ float row_max_across_halves(float x) {
-  return fmaxf(x, __shfl_xor(x, 32, 64));
+__device__ __forceinline__ float as_f(unsigned u) { return __builtin_bit_cast(float, u); }
+__device__ __forceinline__ unsigned as_u(float f) { return __builtin_bit_cast(unsigned, f); }
+
+// Row maxima of two 32-row blocks whose rows are split over lanes l and l^32:
+// returns max(a[l], a[l^32]) in `a` and max(b[l], b[l^32]) in `b`, in every
+// lane.  permlane32_swap(x, y) exchanges the upper half of x with the lower
+// half of y.
+__device__ __forceinline__ void max_halves2(float& a, float& b) {
+  auto r = __builtin_amdgcn_permlane32_swap(as_u(a), as_u(b), false, false);
+  const float u = fmaxf(as_f((unsigned)r[0]), as_f((unsigned)r[1]));  // lanes < 32: block a, else block b
+  auto t = __builtin_amdgcn_permlane32_swap(as_u(u), as_u(u), false, false);
+  a = as_f((unsigned)t[0]);
+  b = as_f((unsigned)t[1]);
 }
 
-__device__ __forceinline__ float row_sum_across_halves(float x) {
-  return x + __shfl_xor(x, 32, 64);
+__device__ __forceinline__ float sum_halves(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(as_u(x), as_u(x), false, false);
+  return as_f((unsigned)r[0]) + as_f((unsigned)r[1]);
 }
+
+// Empty volatile asm that uses and redefines x: keeps the computation of x in
+// the MFMA slot where it is written (the compiler would otherwise sink the
+// softmax arithmetic towards its first use in a later slot or iteration).
+template <typename V>
+__device__ __forceinline__ void pin(V& x) {
+  asm volatile("" : "+v"(x));
+}
+
+// Marks x as used here (no instruction).
+__device__ __forceinline__ void keep_live(const f32x16& x) {
+  asm volatile("" : : "v"(x));
+}
+
+__device__ __forceinline__ void hazard_pad() {
+  // 32 wait states: more than any gfx950 MFMA result latency.
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+
+// Register files.  The S^T accumulators, P and the LDS operands are ordinary
+// values in VGPRs, allocated by the compiler.  O^T, Q, the exp-sums and a
+// constant (1, 1) operand live in fixed AGPRs that only the inline assembly
+// below names: O^T block (rb, db) in a[16 (rb DB + db) .. + 15], Q fragment
+// (rb, kx) in a[128 + 4 (rb KX + kx) .. + 3], l of row block rb in
+// a[192 + 4 rb .. + 3], the ones in a[200 .. 201].
+// Every statement that touches them lists all AGPRs as clobbered, so the
+// compiler keeps none of its own values there, and counts them as used.
+#define ATTN_A10(p) "a" #p "0", "a" #p "1", "a" #p "2", "a" #p "3", "a" #p "4", \
+                    "a" #p "5", "a" #p "6", "a" #p "7", "a" #p "8", "a" #p "9"
+#define ATTN_AGPRS "a0", "a1", "a2", "a3", "a4", "a5", "a6", "a7", "a8", "a9", \
+    ATTN_A10(1), ATTN_A10(2), ATTN_A10(3), ATTN_A10(4), ATTN_A10(5), ATTN_A10(6), ATTN_A10(7), ATTN_A10(8), ATTN_A10(9), ATTN_A10(10), ATTN_A10(11), ATTN_A10(12), ATTN_A10(13), ATTN_A10(14), ATTN_A10(15), ATTN_A10(16), ATTN_A10(17), ATTN_A10(18), ATTN_A10(19), ATTN_A10(20)
+constexpr int kQAgpr = 128;
+constexpr int kLAgpr = 192;     // exp-sum accumulators, 4 per row block
+constexpr int kOnesAgpr = 200;  // two registers holding (1.0, 1.0)
+
+// 32x32x16 MFMAs.  qk0/qk: S^T accumulator in VGPRs (qk0 starts from zero), K
+// operand in VGPRs, Q operand from AGPRs a[QA .. QA + 3].  pv: O^T accumulator
+// a[OA .. OA + 15], both operands in VGPRs.  rowsum: a 4x4x4 MFMA with the
+// all-ones operand, which adds the four 16-bit values each lane holds in b to
+// every register of its accumulator a[LA .. LA + 3]: the exp-sum l is
+// accumulated from the same rounded weights that multiply V, on the matrix
+// unit.  (Its s_nop 1 covers a VALU write of b just before it.)
+template <typename T> struct Mma;
+template <> struct Mma<_Float16> {
+  typedef f16x8 v8;
+  template <int QA> static __device__ __forceinline__ void qk0(f32x16& d, v8 a) {
+    asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  }
+  template <int QA> static __device__ __forceinline__ void qk(f32x16& d, v8 a) {
+    asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  }
+  template <int OA> static __device__ __forceinline__ void pv(v8 a, v8 b) {
+    asm volatile("v_mfma_f32_32x32x16_f16 a[%2:%3], %0, %1, a[%2:%3]" : : "v"(a), "v"(b), "n"(OA), "n"(OA + 15) : ATTN_AGPRS);
+  }
+  static constexpr uint32_t kOnes = 0x3c003c00u;   // (1.0, 1.0)
+  template <int LA> static __device__ __forceinline__ void rowsum(uint2 b) {
+    asm volatile("s_nop 1\n\tv_mfma_f32_4x4x4_16b_f16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
+                 : : "v"(b), "n"(LA), "n"(LA + 3), "n"(kOnesAgpr), "n"(kOnesAgpr + 1) : ATTN_AGPRS);
+  }
+};
+template <> struct Mma<__bf16> {
+  typedef bf16x8 v8;
+  template <int QA> static __device__ __forceinline__ void qk0(f32x16& d, v8 a) {
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  }
+  template <int QA> static __device__ __forceinline__ void qk(f32x16& d, v8 a) {
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  }
+  template <int OA> static __device__ __forceinline__ void pv(v8 a, v8 b) {
+    asm volatile("v_mfma_f32_32x32x16_bf16 a[%2:%3], %0, %1, a[%2:%3]" : : "v"(a), "v"(b), "n"(OA), "n"(OA + 15) : ATTN_AGPRS);
+  }
+  static constexpr uint32_t kOnes = 0x3f803f80u;   // (1.0, 1.0)
+  template <int LA> static __device__ __forceinline__ void rowsum(uint2 b) {
+    asm volatile("s_nop 1\n\tv_mfma_f32_4x4x4_16b_bf16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
+                 : : "v"(b), "n"(LA), "n"(LA + 3), "n"(kOnesAgpr), "n"(kOnesAgpr + 1) : ATTN_AGPRS);
+  }
+};
+
+template <int I>
+__device__ __forceinline__ void agpr_write(uint32_t v) {
+  asm volatile("v_accvgpr_write_b32 a[%1], %0" : : "v"(v), "n"(I) : ATTN_AGPRS);
+}
+template <int I>
+__device__ __forceinline__ void agpr_zero() {
+  asm volatile("v_accvgpr_write_b32 a[%0], 0" : : "n"(I) : ATTN_AGPRS);
+}
+template <int I>
+__device__ __forceinline__ float agpr_read() {
+  float x;
+  asm volatile("v_accvgpr_read_b32 %0, a[%1]" : "=v"(x) : "n"(I));
+  return x;
+}
+template <int I>
+__device__ __forceinline__ void agpr_scale(float s) {
+  float t;
+  asm volatile("v_accvgpr_read_b32 %0, a[%1]\n\tv_mul_f32 %0, %0, %2\n\tv_accvgpr_write_b32 a[%1], %0"
+               : "=&v"(t) : "n"(I), "v"(s) : ATTN_AGPRS);
+}
+
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  [&]<int... Is>(std::integer_sequence<int, Is...>) { (f(std::integral_constant<int, Is>{}), ...); }(
+      std::make_integer_sequence<int, N>{});
+}
+
+// The softmax of one tile as a list of steps, spread over the MFMA slots of
+// an iteration in proportion to their VALU cost (in issue cycles):
+//   prep   4 steps (ALiBi or masked tiles): bias and mask of 4 keys x 2 rows
+//   max    8 steps: 4 scores folded into the partial max of a row block
+//   fin    1 step : row maxima, lazy decisions, repair factors
+//   exp   16 steps: 2 exponentials and their packing
+// (the exp-sum is accumulated by rowsum MFMAs beside P.V).
+template <bool PREP, bool MASKED, bool ALIBI>
+struct SoftPlan {
+  static constexpr int MAX0 = PREP ? 4 : 0;
+  static constexpr int FIN0 = MAX0 + 8;
+  static constexpr int EXP0 = FIN0 + 1;
+  static constexpr int NSTEP = EXP0 + 16;
+  static constexpr int weight(int k) {
+    if (k < MAX0) return (ALIBI ? 12 : 0) * 4 + (MASKED ? 16 : 0) * 4;
+    if (k < FIN0) return 8;
+    if (k < EXP0) return 80;
+    return 30;
+  }
+  // First step of slot s when the steps are spread over ns slots.
+  static constexpr int begin(int s, int ns) {
+    if (s <= 0) return 0;
+    if (s >= ns) return NSTEP;
+    int total = 0;
+    for (int k = 0; k < NSTEP; ++k) total += weight(k);
+    const int target = total * s / ns;
+    int cum = 0, k = 0;
+    while (k < NSTEP && cum < target) cum += weight(k++);
+    return k;
+  }
+};
 
 template <int D, typename T, bool CAUSAL, bool ALIBI>
 struct Prefill {
   typedef Elem<T> E;
+  typedef Mma<T> M;
   typedef typename E::vec8 vec8;
   static constexpr int KX = D / 16;                        // MFMA K-steps of Q.K^T
   static constexpr int DB = D / 32;                        // 32-dim blocks of O^T
   static constexpr int TE = BN * D;                        // elements of one K or V tile
+  static constexpr int NI = TE * (int)sizeof(T) / 1024 / kWaves;  // 1 KB copies per wave per tile
+  static constexpr int CPR = D / 8;                        // 16-byte chunks per row
+  static constexpr int NG = KX;                            // K (or V) operand fragments per tile
+  static_assert(NG == 2 * DB, "as many V fragments as K fragments");
+  static_assert(NI >= 1, "a tile is at least one 1 KB copy per wave");
 
+  // S^T accumulators of one tile: s[rb] holds keys 0..31 of row block rb.
+  // Register r of lane (n, hh) is key 8 (r / 4) + 4 hh + r % 4 of row 32 rb + n.
+  struct Scores {
+    f32x16 s[RB];
+  };
+  // P^T as the B operand of P.V: w[rb][c][..] = keys of 16-key slice c.
+  struct Probs {
+    uint32_t w[RB][2][4];
+  };
   struct State {
-    float m;          // reference max (log2 units of the exponent)
-    float l;          // this lane half's share of the exp-sum
-    f32x16 o[DB];     // O^T accumulators
+    float mc[RB];     // reference max of the row, times ce (log2 units)
+    float alpha[RB];  // pending repair factor of O^T and l
+  };
+  static constexpr int oagpr(int rb, int db) { return 16 * (rb * DB + db); }
+  static constexpr int qagpr(int rb, int kx) { return kQAgpr + 4 * (rb * KX + kx); }
+  // Per-lane LDS byte offsets inside a tile: K fragment kx, V fragment
+  // (c16, db); c16 only adds an immediate.
+  struct Addr {
+    int k[KX];
+    int v[DB][2];
+  };
+  // Softmax scratch of one tile.
+  struct Tmp {
+    float t[RB];
+    uint32_t rep;     // nonzero: some row of this lane needs O^T repaired
+  };
+  struct TileArgs {
+    float c;      // scale * log2(e) (with ALiBi) or max(|scale| * log2(e), tiny)
+    float sl2;    // ALiBi slope * log2(e)
+    float abase;  // ALiBi bias of key j0 + 4 hh relative to the wave's first row
+    int lim[RB];  // last visible key offset (key - j0 - 4 hh) of each row block
   };
 
-  // S^T = K tile . Q^T: s[kb] covers keys 32 kb .. 32 kb + 31.  A operand:
-  // lane (n, hh) reads row 32 kb + n, head dims 16 kx + 8 hh .. + 7.
-  static __device__ __forceinline__ void qk(f32x16 (&s)[2], const T* ks, const vec8 (&qf)[KX], int n, int hh) {
+  // HBM -> LDS copy of key/value tile t (rows t BN .. t BN + BN - 1) of one
+  // head into the LDS slot at byte address `slot`: copy u of wave w fills the
+  // 1 KB block u kWaves + w; dof holds the lane's global byte offsets.  The
+  // buffer range ends at row `rows` (the workgroup's last staged row), so rows
+  // past it read as zero, and a tile past it moves no data at all.  Issued as
+  // inline assembly: the compiler then adds no waits of its own for the LDS
+  // writes; the kernel waits for them explicitly before its barriers.
+  static __device__ __forceinline__ void copy_tile(const T* base, uint32_t slot, int t, int rows, int wave,
+                                                   const int (&dof)[NI]) {
+    const int left = max(rows - t * BN, 0);
+    const uint64_t a = reinterpret_cast<uint64_t>(base + (left > 0 ? (size_t)t * TE : 0));
+    const u32x4 rsrc = {(uint32_t)a, (uint32_t)(a >> 32) & 0xffffu, (uint32_t)(left * D * (int)sizeof(T)), 0x00020000u};
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-#pragma unroll
-    for (int kx = 0; kx < KX; ++kx)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {   // the two accumulator chains alternate
-        const uint4 a = *reinterpret_cast<const uint4*>(ks + lds_off<D>(32 * kb + n, 2 * kx + hh));
-        s[kb] = E::mfma(__builtin_bit_cast(vec8, a), qf[kx], s[kb]);
-      }
-    // Keep kPre K fragments in flight ahead of the MFMA that consumes them.
-    constexpr int kPre = 6;
-    __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
-#pragma unroll
-    for (int g = 0; g < 2 * KX - kPre; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
+    for (int u = 0; u < NI; ++u)
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                   : : "s"(slot + (uint32_t)((u * kWaves + wave) * 1024)), "v"(dof[u]), "s"(rsrc) : "memory", "m0");
   }
 
-  // O^T += V^T P^T.  The A operand (head dims 32 db + m, 16-key slice c16) is
-  // gathered from the row-major V tile with two transposing reads: lane
-  // (m, half hh) receives keys 16 c16 + 4 hh + 0..3 and 16 c16 + 8 + 4 hh + 0..3,
-  // the order in which the S^T accumulator holds keys in the B operand.
-  static __device__ __forceinline__ void pv(State& st, const uint32_t (&pw)[BN / 16][4], const T* vs, int lane) {
+  static __device__ __forceinline__ void make_addr(Addr& ad, int lane) {
+    const int n = lane & 31, hh = lane >> 5;
+#pragma unroll
+    for (int kx = 0; kx < KX; ++kx) ad.k[kx] = 2 * (n * D + 8 * ((2 * kx + hh) ^ swz<D>(n)));
     const int G = lane >> 4, i = lane & 15;
-    const int hh = G >> 1;
 #pragma unroll
-    for (int c16 = 0; c16 < BN / 16; ++c16) {
-      const vec8 bop = __builtin_bit_cast(vec8, make_uint4(pw[c16][0], pw[c16][1], pw[c16][2], pw[c16][3]));
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
+      for (int lh = 0; lh < 2; ++lh) {
         const int d = 32 * db + 16 * (G & 1) + 4 * (i & 3);   // this source lane's 4 head dims
-        const int k = 16 * c16 + 4 * hh + (i >> 2);            // this source lane's key
-        const uint2 lo = lds_read_tr(vs + lds_off<D>(k, d >> 3) + (d & 7));
-        const uint2 hi = lds_read_tr(vs + lds_off<D>(k + 8, d >> 3) + (d & 7));
-        const vec8 a = __builtin_bit_cast(vec8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-        st.o[db] = E::mfma(a, bop, st.o[db]);
+        const int k = 4 * (G >> 1) + (i >> 2) + 8 * lh;        // this source lane's key in the slice
+        ad.v[db][lh] = 2 * (k * D + 8 * ((d >> 3) ^ swz<D>(k)) + (d & 7));
       }
-    }
-    // Keep four operands (eight transposing reads) in flight ahead of the MFMAs.
-    constexpr int kPre = 4;
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPre, 0);
-#pragma unroll
-    for (int g = 0; g < DB * (BN / 16) - kPre; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
   }
 
-  // Softmax of one tile: rolling update of the reference max and l, P packed
-  // for the P.V MFMA.  Returns whether the reference max moved (then `alpha`
-  // is the repair factor of O^T).  Register r of block kb holds key
-  // j0 + 32 kb + 8 (r / 4) + 4 hh + r % 4 of row `row`.
-  template <bool MASKED>
-  static __device__ __forceinline__ bool softmax(State& st, f32x16 (&s)[2], uint32_t (&pw)[BN / 16][4],
-                                                 float& alpha, const float c, const float sl2, int j0, int row,
-                                                 int off, int Lk, int hh) {
-    const float ce = ALIBI ? 1.f : c;
-    float base = 0.f;
-    if (ALIBI) base = sl2 * (float)(j0 + 4 * hh - (row + off));
-    float tmax = kNegInf;
+  // K operand kx: lane (n, hh) reads key n, head dims 16 kx + 8 hh .. + 7.
+  static __device__ __forceinline__ vec8 kfrag(const T* tile, const Addr& ad, int kx) {
+    return __builtin_bit_cast(vec8, *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(tile) + ad.k[kx]));
+  }
+
+  // V^T operand g (head dims 32 db + m, 16-key slice c16, g = c16 DB + db):
+  // lane (m, half hh) receives keys 16 c16 + 4 hh + 0..3 and 16 c16 + 8 + 4 hh
+  // + 0..3, the order in which the S^T accumulator holds keys in the B operand.
+  static __device__ __forceinline__ vec8 vfrag(const T* tile, const Addr& ad, int g) {
+    const char* base = reinterpret_cast<const char*>(tile) + (g / DB) * 32 * D;
+    const uint2 lo = lds_read_tr(base + ad.v[g % DB][0]);
+    const uint2 hi = lds_read_tr(base + ad.v[g % DB][1]);
+    return __builtin_bit_cast(vec8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+  }
+
+  static __device__ __forceinline__ vec8 probs_b(const Probs& pr, int rb, int c16) {
+    return __builtin_bit_cast(vec8, make_uint4(pr.w[rb][c16][0], pr.w[rb][c16][1], pr.w[rb][c16][2], pr.w[rb][c16][3]));
+  }
+
+  static constexpr int kconst(int r) { return 8 * (r / 4) + (r % 4); }
+
+  // Softmax step K of a tile (see SoftPlan).  Without ALiBi the exponent is
+  // s * c - m * c.  With ALiBi the score is first made s * c + bias in log2
+  // units; the bias is written relative to the wave's first row,
+  // -slope (i - j) = slope (j - iw - off) - slope (i - iw), and the last term
+  // is dropped: it shifts a whole row by a constant, which the row's softmax
+  // does not see.  Masked tiles set keys past Lk and (causal) keys after the
+  // row to -inf before the max.
+  template <int K, bool PREP, bool MASKED>
+  static __device__ __forceinline__ void soft_step(State& st, Scores& sc, Probs& pr, Tmp& tp, const TileArgs& ta) {
+    typedef SoftPlan<PREP, MASKED, ALIBI> P;
+    const float ce = ALIBI ? 1.f : ta.c;
+    if constexpr (K < P::MAX0) {
+      constexpr int r0 = 4 * K;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int r = r0; r < r0 + 4; ++r) {
+        if constexpr (ALIBI) {
+          const float bias = __builtin_fmaf(ta.sl2, (float)kconst(r), ta.abase);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = s[kb][r];
-        if (ALIBI) x = __builtin_fmaf(x, c, __builtin_fmaf(sl2, (float)(32 * kb + 8 * (r / 4) + (r % 4)), base));
-        if (MASKED) {
-          const int j = j0 + 32 * kb + 8 * (r / 4) + 4 * hh + (r % 4);
-          if (j >= Lk || (CAUSAL && j > row + off)) x = kNegInf;
+          for (int rb = 0; rb < RB; ++rb) sc.s[rb][r] = __builtin_fmaf(sc.s[rb][r], ta.c, bias);
         }
-        s[kb][r] = x;
-        tmax = fmaxf(tmax, x);
+        if constexpr (MASKED) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            if (kconst(r) > ta.lim[rb]) sc.s[rb][r] = kNegInf;
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          float x = sc.s[rb][r];
+          pin(x);
+          sc.s[rb][r] = x;
+        }
       }
-    tmax = row_max_across_halves(tmax);
-    const float m = st.m;
-    const bool move = (m == kNegInf) ? (tmax != kNegInf) : ((tmax - m) * ce > kLazyThreshold);
-    float a = 1.f, mref = m;
-    if (move) {
-      a = (m == kNegInf) ? 0.f : fast_exp2((m - tmax) * ce);
-      mref = tmax;
+    } else if constexpr (K < P::FIN0) {
+      constexpr int k = K - P::MAX0;
+      constexpr int q = k / 2, rb = k % 2;
+      const f32x16& s = sc.s[rb];
+      const float m4 = fmaxf(fmaxf(s[4 * q], s[4 * q + 1]), fmaxf(s[4 * q + 2], s[4 * q + 3]));
+      if constexpr (q == 0) tp.t[rb] = m4;
+      else tp.t[rb] = fmaxf(tp.t[rb], m4);
+      pin(tp.t[rb]);
+    } else if constexpr (K < P::EXP0) {
+      float t0 = tp.t[0], t1 = tp.t[1];
+      max_halves2(t0, t1);
+      const float tm[RB] = {t0, t1};
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const float d = __builtin_fmaf(tm[rb], ce, -st.mc[rb]);   // how far the tile max is above the reference
+        const bool move = d > kLazyThreshold;
+        tp.rep |= (move && st.mc[rb] > kMcFresh) ? 1u : 0u;
+        st.alpha[rb] = move ? fast_exp2(-d) : 1.f;
+        st.mc[rb] = move ? tm[rb] * ce : st.mc[rb];
+        pin(st.alpha[rb]);
+        pin(st.mc[rb]);
+      }
+      pin(tp.rep);
+    } else {
+      constexpr int k = K - P::EXP0;
+      constexpr int rb = k % 2, r = 2 * (k / 2);
+      const float p0 = fast_exp2(__builtin_fmaf(sc.s[rb][r], ce, -st.mc[rb]));
+      const float p1 = fast_exp2(__builtin_fmaf(sc.s[rb][r + 1], ce, -st.mc[rb]));
+      uint32_t w = E::pack2(p0, p1);
+      pin(w);
+      pr.w[rb][r / 8][(r % 8) / 2] = w;
     }
-    st.m = mref;
-    alpha = a;
-    const float mc = (mref == kNegInf) ? 0.f : mref * ce;
-    // The row sum adds the fp32 weights (two partial sums); the packed dot
-    // product would sum the rounded weights exactly, but it blocks the MFMA
-    // pipe for far longer than plain adds on gfx950.
-    float lsum0 = 0.f, lsum1 = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        float p0 = fast_exp2(__builtin_fmaf(s[kb][r], ce, -mc));
-        float p1 = fast_exp2(__builtin_fmaf(s[kb][r + 1], ce, -mc));
-        if (MASKED) {
-          p0 = s[kb][r] == kNegInf ? 0.f : p0;
-          p1 = s[kb][r + 1] == kNegInf ? 0.f : p1;
-        }
-        lsum0 += p0;
-        lsum1 += p1;
-        pw[2 * kb + r / 8][(r % 8) / 2] = E::pack2(p0, p1);
+  }
+
+  template <int B0, int B1, bool PREP, bool MASKED>
+  static __device__ __forceinline__ void soft_range(State& st, Scores& sc, Probs& pr, Tmp& tp, const TileArgs& ta) {
+    if constexpr (B1 > B0) {
+      [&]<int... Ks>(std::integer_sequence<int, Ks...>) {
+        (soft_step<B0 + Ks, PREP, MASKED>(st, sc, pr, tp, ta), ...);
+      }(std::make_integer_sequence<int, B1 - B0>{});
+    }
+  }
+
+  // One iteration of the software pipeline: S^T of tile j+1 (QK), softmax of
+  // tile j (SM: 0 none, 1 unmasked, 2 masked), P.V of tile j-1 (PV).  Group g
+  // holds the slots [QK rb 0, QK rb 1, PV rb 0, PV rb 1] of K fragment g and V
+  // fragment g (the parts present); each fragment is read from LDS PFD
+  // fragments ahead of its first slot.
+  template <bool QK, int SM, bool PV>
+  static __device__ __forceinline__ bool iterate(State& st, Scores& s_cur, Scores& s_next, Probs& p_cur,
+                                                 const Probs& p_prev, const T* kl, const T* vl, const Addr& ad,
+                                                 const TileArgs& ta) {
+    constexpr bool MASKED = SM == 2;
+    constexpr bool PREP = ALIBI || MASKED;
+    typedef SoftPlan<PREP, MASKED, ALIBI> P;
+    constexpr int FPG = (QK ? 1 : 0) + (PV ? 1 : 0);   // fragments per group
+    constexpr int NF = NG * FPG;                        // fragments of the iteration
+    constexpr int NS = 2 * NF;                          // MFMA slots
+    Tmp tp;
+    tp.rep = 0;
+    vec8 fr[PFD + 1];
+    // Fragment i of the iteration: group i / FPG, K first when both.
+    auto read = [&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (i < NF) {
+        constexpr int g = i / FPG;
+        constexpr bool is_k = QK && (i % FPG == 0);
+        if constexpr (is_k) fr[i % (PFD + 1)] = kfrag(kl, ad, g);
+        else fr[i % (PFD + 1)] = vfrag(vl, ad, g);
       }
-    const float lsum = lsum0 + lsum1;
-    st.l = __builtin_fmaf(st.l, a, lsum);
-    return move;
+    };
+    if constexpr (NS == 0) {
+      if constexpr (SM != 0) soft_range<0, P::NSTEP, PREP, MASKED>(st, s_cur, p_cur, tp, ta);
+    } else {
+      [&]<int... Is>(std::integer_sequence<int, Is...>) {
+        (read(std::integral_constant<int, Is>{}), ...);
+      }(std::make_integer_sequence<int, PFD>{});
+      [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
+        (
+            [&] {
+              constexpr int S = Ss;
+              constexpr int i = S / 2, rb = S % 2;
+              constexpr int g = i / FPG;
+              constexpr bool is_k = QK && (i % FPG == 0);
+              if constexpr (rb == 0) read(std::integral_constant<int, i + PFD>{});
+              if constexpr (is_k) {
+                if constexpr (g == 0) M::template qk0<qagpr(rb, g)>(s_next.s[rb], fr[i % (PFD + 1)]);
+                else M::template qk<qagpr(rb, g)>(s_next.s[rb], fr[i % (PFD + 1)]);
+              } else {
+                constexpr int c16 = g / DB, db = g % DB;
+                M::template pv<oagpr(rb, db)>(fr[i % (PFD + 1)], probs_b(p_prev, rb, c16));
+                // Exp-sum of the same weights: words 2 db, 2 db + 1 of the
+                // slice, at fragments db = 0 and 1 (a large MFMA always
+                // separates two rowsum MFMAs on one accumulator).
+                if constexpr (db < 2)
+                  M::template rowsum<kLAgpr + 4 * rb>(
+                      make_uint2(p_prev.w[rb][c16][2 * db], p_prev.w[rb][c16][2 * db + 1]));
+              }
+              if constexpr (SM != 0)
+                soft_range<P::begin(S, NS), P::begin(S + 1, NS), PREP, MASKED>(st, s_cur, p_cur, tp, ta);
+              __builtin_amdgcn_sched_barrier(0);
+            }(),
+            ...);
+      }(std::make_integer_sequence<int, NS>{});
+    }
+    return tp.rep != 0;
+  }
+
+  // O^T *= alpha and l *= alpha, in place in the AGPRs.
+  static __device__ __forceinline__ void repair(const State& st) {
+    hazard_pad();
+    static_for<RB * DB * 16>([&](auto ic) {
+      constexpr int e = decltype(ic)::value;
+      agpr_scale<e>(st.alpha[e / (16 * DB)]);
+    });
+    static_for<RB * 4>([&](auto ic) {
+      constexpr int e = decltype(ic)::value;
+      agpr_scale<kLAgpr + e>(st.alpha[e / 4]);
+    });
+    hazard_pad();
   }
 };
 
@@ -226,11 +524,16 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   typedef Prefill<D, T, CAUSAL, ALIBI> PF;
   typedef typename PF::vec8 vec8;
   typedef typename PF::State State;
+  typedef typename PF::Scores Scores;
+  typedef typename PF::Probs Probs;
+  typedef typename PF::Addr Addr;
+  typedef typename PF::TileArgs TileArgs;
   constexpr int KX = PF::KX;
   constexpr int TE = PF::TE;
-  constexpr int CH = BN * D / 8 / kThreads;   // 16-byte chunks of one tile per thread
-  // [K buf 0][K buf 1][V buf 0][V buf 1]
-  __shared__ __attribute__((aligned(16))) T smem[4 * TE];
+  constexpr int NI = PF::NI;
+  constexpr int CPR = PF::CPR;
+  // LDS: a ring of kRing K tiles, then a ring of kRing V tiles.
+  __shared__ __attribute__((aligned(1024))) T lds[2 * kRing * TE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -238,171 +541,244 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   const int n = lane & 31;
   const int hh = lane >> 5;
 
-  // Workgroup -> (query block, head); consecutive logical blocks share an XCD,
-  // and within a head the query blocks with the most keys run first.
-  int bid = blockIdx.x;
-  if (p.xcd_remap) bid = (bid & 7) * (gridDim.x >> 3) + (bid >> 3);
-  const int head = bid / p.nqb;
-  const int qb = p.nqb - 1 - (bid - head * p.nqb);
-  const int b = head / p.Hq;
-  const int hq = head - b * p.Hq;
-  const int hk = hq / p.group;
-  const int Lq = p.Lq, Lk = p.Lk;
-  const int off = Lk - Lq;
-  const int i0 = qb * BM;
-  const int iw = i0 + 32 * wave;   // first row of this wave
-  const int row = iw + n;          // this lane's row
-
-  // Tiles: the workgroup stages [0, n_wg); this wave computes [0, n_w); tiles
-  // [0, fm_w) need no mask for any of its rows.
-  int kend = Lk, kend_w = Lk;
-  if (CAUSAL) {
-    kend = min(Lk, min(i0 + BM, Lq) + off);
-    kend_w = min(Lk, min(iw + 32, Lq) + off);
+  Addr ad;
+  PF::make_addr(ad, lane);
+  // Global offsets of this lane's HBM -> LDS copies: in copy u the lane writes
+  // bytes 16 lane .. 16 lane + 15 of 1 KB block u * kWaves + wave, i.e. chunk
+  // position lane % CPR of row (block * 1024 / (2 D) + lane / CPR), and reads
+  // the global chunk that the swizzle puts there.
+  int dof[NI];
+#pragma unroll
+  for (int u = 0; u < NI; ++u) {
+    const int blk = u * kWaves + wave;
+    const int r = blk * (1024 / (2 * D)) + lane / CPR;
+    const int pos = lane % CPR;
+    dof[u] = (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T);
   }
-  if (iw >= Lq) kend_w = 0;
-  const int n_wg = kend > 0 ? (kend + BN - 1) / BN : 0;
-  const int n_w = kend_w > 0 ? (kend_w + BN - 1) / BN : 0;
-  int fm_w = Lk / BN;
-  if (CAUSAL) fm_w = min(fm_w, max(0, (iw + off + 1) / BN));
-  fm_w = min(fm_w, n_w);
-
-  const T* qp = reinterpret_cast<const T*>(p.q) + (size_t)head * Lq * D;
-  const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)(b * p.Hkv + hk) * Lk * D;
-  const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)(b * p.Hkv + hk) * Lk * D;
-
-  // Q fragments (B operand of S^T): lane (n, hh) holds Q[row][16 kx + 8 hh + 0..7].
-  vec8 qf[KX];
-#pragma unroll
-  for (int kx = 0; kx < KX; ++kx) {
-    uint4 w = make_uint4(0, 0, 0, 0);
-    if (row < Lq) w = *reinterpret_cast<const uint4*>(qp + (size_t)row * D + 16 * kx + 8 * hh);
-    w.x ^= p.qsign; w.y ^= p.qsign; w.z ^= p.qsign; w.w ^= p.qsign;
-    qf[kx] = __builtin_bit_cast(vec8, w);
-  }
-
-  T* const kbuf = smem;
-  T* const vbuf = smem + 2 * TE;
-
-  // Staging of K and V tiles through registers, one tile ahead: thread t owns
-  // chunks idx = c * 512 + t (row idx / (D/8), chunk idx % (D/8)), so 16
-  // lanes read one 256-byte row.  Loads go through buffer resources bounded
-  // at the head's Lk rows: rows past Lk read as zero (such keys are always
-  // masked), and the per-lane offsets are loop invariant.
-  const __amdgpu_buffer_rsrc_t krs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(kp), (short)0, Lk * D * (int)sizeof(T), 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(vp), (short)0, Lk * D * (int)sizeof(T), 0x00020000);
-  int goff[CH], loff[CH];
-#pragma unroll
-  for (int c = 0; c < CH; ++c) {
-    const int idx = c * kThreads + tid;
-    const int r = idx / (D / 8), ch = idx % (D / 8);
-    goff[c] = (r * D + ch * 8) * (int)sizeof(T);
-    loff[c] = lds_off<D>(r, ch);
-  }
-  u32x4 kst[CH], vst[CH];
-  // The tile offset is folded into the per-lane (VGPR) offset, which the
-  // buffer range check covers, so rows at or past Lk read as zero.
-  auto sload = [&](int t) {
-    const unsigned tk = (unsigned)t * (unsigned)(BN * D * sizeof(T));
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      kst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(krs, (int)(tk + goff[c]), 0, 0));
-      vst[c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vrs, (int)(tk + goff[c]), 0, 0));
-    }
-  };
-  auto sstore = [&](int par) {
-    T* kd = kbuf + par * TE;
-    T* vd = vbuf + par * TE;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      *reinterpret_cast<u32x4*>(kd + loff[c]) = kst[c];
-      *reinterpret_cast<u32x4*>(vd + loff[c]) = vst[c];
-    }
+  // LDS byte addresses of the K and V slots.
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)lds;
+  auto kslot = [&](int s) __attribute__((always_inline)) { return lds0 + (uint32_t)(s * TE * (int)sizeof(T)); };
+  auto vslot = [&](int s) __attribute__((always_inline)) {
+    return lds0 + (uint32_t)((kRing + s) * TE * (int)sizeof(T));
   };
 
-  State st;
-  st.m = kNegInf;
-  st.l = 0.f;
-#pragma unroll
-  for (int db = 0; db < PF::DB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) st.o[db][r] = 0.f;
+  // Persistent workgroups.  Work item s is (query block, head) with the query
+  // blocks ordered by decreasing key count: s / nheads-th heaviest block of
+  // head s % nheads.  Round r gives item r * P + g to workgroup g on even
+  // rounds and r * P + P - 1 - g on odd ones (P workgroups), so that the
+  // heaviest and lightest blocks pair up and, with causal masking (key
+  // counts falling linearly with the block index), every workgroup gets the
+  // same number of key tiles.
+  const int P = gridDim.x;
+  const int wg = blockIdx.x;
+  for (int round = 0;; ++round) {
+    const int s = round * P + ((round & 1) ? P - 1 - wg : wg);
+    if (s >= p.nitems) break;
+    const int head = s % p.nheads;
+    const int qb = p.nqb - 1 - s / p.nheads;
+    const int b = head / p.Hq;
+    const int hq = head - b * p.Hq;
+    const int hk = hq / p.group;
+    const int Lq = p.Lq, Lk = p.Lk;
+    const int off = Lk - Lq;
+    const int i0 = qb * BM;
+    const int iw = i0 + BMW * wave;   // first row of this wave
+    const int row0 = iw + n;          // this lane's row in row block 0
 
-  const float c = p.c;
-  float sl2 = 0.f;
-  if (ALIBI) sl2 = p.slopes[hq] * kLog2e;
+    // Tiles: the workgroup stages [0, nt); this wave computes [0, n_w); tiles
+    // [0, fm_w) need no mask for any of its rows.
+    int kend = Lk, kend_w = Lk;
+    if (CAUSAL) {
+      kend = min(Lk, min(i0 + BM, Lq) + off);
+      kend_w = min(Lk, min(iw + BMW, Lq) + off);
+    }
+    if (iw >= Lq) kend_w = 0;
+    const int nt = kend > 0 ? (kend + BN - 1) / BN : 0;
+    const int n_w = kend_w > 0 ? (kend_w + BN - 1) / BN : 0;
+    int fm_w = Lk / BN;
+    if (CAUSAL) fm_w = min(fm_w, max(0, (iw + off + 1) / BN));
+    fm_w = min(fm_w, n_w);
 
-  f32x16 s[2];
-  uint32_t pw[BN / 16][4];
+    const T* qp = reinterpret_cast<const T*>(p.q) + (size_t)head * Lq * D;
+    const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)(b * p.Hkv + hk) * Lk * D;
+    const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)(b * p.Hkv + hk) * Lk * D;
 
-  if (n_wg > 0) {
-    sload(0);
-    sstore(0);
-    sload(1);
-  }
-  __syncthreads();
-
-  // Tile j lives in LDS buffer pair j & 1; the loop is unrolled by two so the
-  // buffer offsets are compile-time constants.
-  auto step = [&](int j, auto parity) {
-    constexpr int par = decltype(parity)::value;
-    const T* kc = kbuf + par * TE;
-    const T* vc = vbuf + par * TE;
-    if (j < n_w) {
-      PF::qk(s, kc, qf, n, hh);
-      float alpha = 1.f;
-      bool moved;
-      if (j < fm_w)
-        moved = PF::template softmax<false>(st, s, pw, alpha, c, sl2, j * BN, row, off, Lk, hh);
-      else
-        moved = PF::template softmax<true>(st, s, pw, alpha, c, sl2, j * BN, row, off, Lk, hh);
-      if (moved) {
+    State st;
+    // Q fragments (B operand of S^T): lane (n, hh) holds Q[row][16 kx + 8 hh + 0..7],
+    // written once into their AGPRs; O^T starts at zero.
+    static_for<RB * KX>([&](auto ic) {
+      constexpr int f = decltype(ic)::value;
+      constexpr int rb = f / KX, kx = f % KX;
+      const int row = row0 + 32 * rb;
+      uint4 w = make_uint4(0, 0, 0, 0);
+      if (row < Lq) w = *reinterpret_cast<const uint4*>(qp + (size_t)row * D + 16 * kx + 8 * hh);
+      agpr_write<PF::qagpr(rb, kx) + 0>(w.x ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 1>(w.y ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 2>(w.z ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 3>(w.w ^ p.qsign);
+    });
+    static_for<RB * PF::DB * 16>([&](auto ic) { agpr_zero<decltype(ic)::value>(); });
+    static_for<RB * 4>([&](auto ic) { agpr_zero<kLAgpr + decltype(ic)::value>(); });
+    agpr_write<kOnesAgpr>(PF::M::kOnes);
+    agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
 #pragma unroll
-        for (int db = 0; db < PF::DB; ++db)
+    for (int rb = 0; rb < RB; ++rb) {
+      st.mc[rb] = kMcInit;
+      st.alpha[rb] = 1.f;
+    }
+    const int rows = min(Lk, nt * BN);
+    auto copy_tile = [&](const T* base, uint32_t slot, int t) __attribute__((always_inline)) {
+      PF::copy_tile(base, slot, t, rows, wave, dof);
+    };
+
+    TileArgs ta;
+    ta.c = p.c;
+    ta.sl2 = ALIBI ? p.slopes[hq] * kLog2e : 0.f;
+    // Per-tile softmax parameters.  Tiles outside [0, n_w) are fully masked
+    // (lim = -1): their softmax leaves the state unchanged and gives P = 0.
+    auto set_tile = [&](int j) __attribute__((always_inline)) {
+      const int j0 = j * BN;
+      ta.abase = ALIBI ? ta.sl2 * (float)(j0 + 4 * hh - iw - off) : 0.f;
+      const bool live = j >= 0 && j < n_w;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) st.o[db][r] *= alpha;
+      for (int rb = 0; rb < RB; ++rb) {
+        int l = Lk - 1 - j0 - 4 * hh;
+        if (CAUSAL) l = min(l, row0 + 32 * rb + off - j0 - 4 * hh);
+        ta.lim[rb] = live ? l : -1;
       }
-      PF::pv(st, pw, vc, lane);
-    }
-    // Tile j+1 goes into the other buffer pair (last read in step j-1); then
-    // the loads of tile j+2 are issued and stay in flight across the barrier.
-    if (j + 1 < n_wg) sstore(par ^ 1);
-    sload(j + 2);
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  };
-  int j = 0;
-  for (; j + 1 < n_wg; j += 2) {
-    step(j, std::integral_constant<int, 0>{});
-    step(j + 1, std::integral_constant<int, 1>{});
-  }
-  if (j < n_wg) step(j, std::integral_constant<int, 0>{});
+    };
 
-  // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
-  // head dims 32 db + 8 g + 4 hh + 0..3 of its row.
-  const float lt = row_sum_across_halves(st.l);
-  const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (row < Lq) {
-    T* op = reinterpret_cast<T*>(p.o) + ((size_t)head * Lq + row) * D;
+    Scores sc[2];
+    Probs pr[2];
+    // P of tile -2 is zero.  Pinned, so that the zeros are materialised in
+    // VGPRs here and not just before the first P.V MFMA that reads them.
 #pragma unroll
-    for (int db = 0; db < PF::DB; ++db)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        uint2 w;
-        w.x = PF::E::pack2(st.o[db][4 * g] * inv, st.o[db][4 * g + 1] * inv);
-        w.y = PF::E::pack2(st.o[db][4 * g + 2] * inv, st.o[db][4 * g + 3] * inv);
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          uint32_t z = 0u;
+          pin(z);
+          pr[0].w[rb][c][w] = z;
+        }
+
+    // Iteration j (from -1): copies of K_{j+kRing} and V_{j+kRing-2}; S^T of
+    // tile j+1, softmax of tile j, P.V of tile j-1, then the pending repair of
+    // O^T.  Tile t of K or V lives in slot t mod kRing: a copy is issued
+    // kRing - 1 iterations before the tile's first use, into the slot read by
+    // the iteration before, and waited for only at the end of the iteration
+    // before its use (vmcnt allows the copies of the last two iterations to
+    // be in flight; every iteration issues the same number of copies).  The
+    // scores and probabilities of tile j live in the register buffers of the
+    // parity of j.  VAR is 1 for tiles every row of the wave sees whole, 2 for
+    // masked tiles (including the tiles outside [0, n_w), whose softmax is a
+    // no-op: P = 0, K unused), 0 for waves that have run out of tiles (copies
+    // and barrier only).
+    auto iteration = [&](int j, auto var, auto slotc) __attribute__((always_inline)) {
+      constexpr int VAR = decltype(var)::value;
+      constexpr int k = decltype(slotc)::value;   // j mod kRing
+      constexpr int par = k & 1;
+      copy_tile(kp, kslot(k), j + kRing);
+      copy_tile(vp, vslot((k + kRing - 2) % kRing), j + kRing - 2);
+      if constexpr (VAR != 0) {
+        set_tile(j);
+        const T* kl_use = lds + ((k + 1) % kRing) * TE;                  // K_{j+1}
+        const T* vl_use = lds + (kRing + (k + kRing - 1) % kRing) * TE;  // V_{j-1}
+        const bool rep = PF::template iterate<true, VAR, true>(st, sc[par], sc[par ^ 1], pr[par], pr[par ^ 1], kl_use,
+                                                               vl_use, ad, ta);
+        if (__builtin_amdgcn_ballot_w64(rep) != 0) PF::repair(st);
+      }
+      // 16 wait states between this iteration's last MFMAs and the next
+      // iteration's first reads of their results; the copies of all but the
+      // last two iterations complete; then the barrier publishes them.
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(4 * NI) : "memory");
+    };
+    // Iterations j in [j0, j1), j0 >= 0, of one variant; the loop body is
+    // unrolled by kRing so that slots and parities are compile-time choices.
+    // Every iteration of every wave ends in one barrier, so the waves of the
+    // workgroup stay in step whatever their phase boundaries.
+    auto phase = [&](int j0, int j1, auto var) __attribute__((always_inline)) {
+      for (int jb = j0 & ~(kRing - 1); jb < j1; jb += kRing) {
+        static_for<kRing>([&](auto kc) __attribute__((always_inline)) {
+          const int j = jb + decltype(kc)::value;
+          if (j >= j0 && j < j1) iteration(j, var, kc);
+        });
+      }
+    };
+
+    // Prologue: K_0 .. K_{kRing-2} and V_0 in flight, the V slots of tiles -1 and
+    // -2 zeroed (the first two iterations multiply them by P = 0).
+    {
+      constexpr int NV16 = TE * (int)sizeof(T) / 16;
+      uint4* vz = reinterpret_cast<uint4*>(lds + (kRing + kRing - 2) * TE);   // slots kRing-2, kRing-1
+#pragma unroll
+      for (int i = tid; i < 2 * NV16; i += kThreads) vz[i] = make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < kRing - 1; ++t) copy_tile(kp, kslot(t), t);
+    copy_tile(vp, vslot(0), 0);
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    const int m0 = max(fm_w, 0);
+    iteration(-1, std::integral_constant<int, 2>{}, std::integral_constant<int, kRing - 1>{});
+    phase(0, fm_w, std::integral_constant<int, 1>{});
+    phase(m0, n_w + 1, std::integral_constant<int, 2>{});
+    phase(n_w + 1, nt + 1, std::integral_constant<int, 0>{});
+
+    // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
+    // head dims 32 db + 8 g + 4 hh + 0..3 of its row.  The scores of the last
+    // iteration are dead, but are kept live past the padding so that their
+    // registers are not reused while the MFMAs writing them are in flight.
+    hazard_pad();
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) keep_live(sc[pb].s[rb]);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const float lt = sum_halves(rb == 0 ? agpr_read<kLAgpr>() : agpr_read<kLAgpr + 4>());
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+      st.alpha[rb] = inv;
+    }
+    static_for<RB * PF::DB * 4>([&](auto ic) {
+      constexpr int f = decltype(ic)::value;
+      constexpr int rb = f / (PF::DB * 4), db = (f / 4) % PF::DB, g = f % 4;
+      constexpr int a0 = PF::oagpr(rb, db) + 4 * g;
+      const float inv = st.alpha[rb];
+      uint2 w;
+      w.x = PF::E::pack2(agpr_read<a0>() * inv, agpr_read<a0 + 1>() * inv);
+      w.y = PF::E::pack2(agpr_read<a0 + 2>() * inv, agpr_read<a0 + 3>() * inv);
+      const int row = row0 + 32 * rb;
+      if (row < Lq) {
+        T* op = reinterpret_cast<T*>(p.o) + ((size_t)head * Lq + row) * D;
         *reinterpret_cast<uint2*>(op + 32 * db + 8 * g + 4 * hh) = w;
       }
+    });
   }
+}
+
+// Compute units of the current device: one persistent workgroup each.
+int compute_units() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
 }
 
 template <int D, typename T, bool CAUSAL, bool ALIBI>
 hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
-  const int nblocks = p.nqb * p.B * p.Hq;
   PrefillParams q = p;
-  q.xcd_remap = (nblocks % 8 == 0) ? 1 : 0;
-  hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI>), dim3(nblocks), dim3(kThreads), 0, stream, q);
+  q.nheads = p.B * p.Hq;
+  q.nitems = p.nqb * q.nheads;
+  if (q.nitems == 0) return hipSuccess;
+  const int grid = std::min(q.nitems, compute_units());
+  hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI>), dim3(grid), dim3(kThreads), 0, stream, q);
   return hipGetLastError();
 }
 
@@ -416,11 +792,29 @@ hipError_t launch_d(const PrefillParams& p, hipStream_t s) {
 
 }  // namespace
 
+// This file is compiled once per (head dim, element type) shard, selected by
+// ATTN_PREFILL_SHARD, so the instantiations build in parallel; shard 0 also
+// holds the dispatcher.
+#ifndef ATTN_PREFILL_SHARD
+#define ATTN_PREFILL_SHARD 0
+#endif
+#if ATTN_PREFILL_SHARD == 0
+hipError_t launch_prefill_d128_f16(const PrefillParams& p, hipStream_t s) { return launch_d<128, _Float16>(p, s); }
+#elif ATTN_PREFILL_SHARD == 1
+hipError_t launch_prefill_d128_bf16(const PrefillParams& p, hipStream_t s) { return launch_d<128, __bf16>(p, s); }
+#elif ATTN_PREFILL_SHARD == 2
+hipError_t launch_prefill_d64_f16(const PrefillParams& p, hipStream_t s) { return launch_d<64, _Float16>(p, s); }
+#elif ATTN_PREFILL_SHARD == 3
+hipError_t launch_prefill_d64_bf16(const PrefillParams& p, hipStream_t s) { return launch_d<64, __bf16>(p, s); }
+#endif
+
+#if ATTN_PREFILL_SHARD == 0
 int prefill_block_rows() { return BM; }
 
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
-  if (p.D == 64) return p.bf16 ? launch_d<64, __bf16>(p, stream) : launch_d<64, _Float16>(p, stream);
-  return p.bf16 ? launch_d<128, __bf16>(p, stream) : launch_d<128, _Float16>(p, stream);
+  if (p.D == 64) return p.bf16 ? launch_prefill_d64_bf16(p, stream) : launch_prefill_d64_f16(p, stream);
+  return p.bf16 ? launch_prefill_d128_bf16(p, stream) : launch_prefill_d128_f16(p, stream);
 }
+#endif
 
 }  // namespace attn
