@@ -21,6 +21,7 @@ struct PrefillParams {
   int nqb;              // query blocks per head
   int nheads;           // B * Hq, set by the launcher
   int nitems;           // nqb * nheads, set by the launcher
+  int nxcd;             // XCDs the workgroups are spread over, set by the launcher
 };
 
 struct DecodeParams {

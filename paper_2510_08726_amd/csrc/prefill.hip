@@ -80,6 +80,9 @@ constexpr float kLazyThreshold = 8.f;       // log2 units
 // Reference max (times c) before the first visible key: finite, so the first
 // tile's decision and repair factor need no special case (its repair factor
 // underflows to 0, and O^T and l are still 0 then).
+// Accelerator dies (XCDs), each with its own L2; consecutive workgroups of a
+// launch are dealt to them in turn.
+constexpr int kXcds = 8;
 constexpr float kMcInit = -1e30f;
 constexpr float kMcFresh = -1e29f;
 
@@ -319,9 +322,13 @@ struct Prefill {
   // writes; the kernel waits for them explicitly before its barriers.
   static __device__ __forceinline__ void copy_tile(const T* base, uint32_t slot, int t, int rows, int wave,
                                                    const int (&dof)[NI]) {
-    const int left = max(rows - t * BN, 0);
+    const int left = t >= 0 ? max(rows - t * BN, 0) : 0;
     const uint64_t a = reinterpret_cast<uint64_t>(base + (left > 0 ? (size_t)t * TE : 0));
-    const u32x4 rsrc = {(uint32_t)a, (uint32_t)(a >> 32) & 0xffffu, (uint32_t)(left * D * (int)sizeof(T)), 0x00020000u};
+    // The words are uniform; readfirstlane keeps them in SGPRs even where the
+    // compiler computes the 64-bit address with vector instructions.
+    const u32x4 rsrc = {(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
+                        (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
+                        (uint32_t)__builtin_amdgcn_readfirstlane(left * D * (int)sizeof(T)), 0x00020000u};
 #pragma unroll
     for (int u = 0; u < NI; ++u)
       asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
@@ -522,6 +529,7 @@ struct Prefill {
 template <int D, typename T, bool CAUSAL, bool ALIBI>
 __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   typedef Prefill<D, T, CAUSAL, ALIBI> PF;
+  constexpr bool REV = ALIBI;
   typedef typename PF::vec8 vec8;
   typedef typename PF::State State;
   typedef typename PF::Scores Scores;
@@ -562,20 +570,32 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     return lds0 + (uint32_t)((kRing + s) * TE * (int)sizeof(T));
   };
 
-  // Persistent workgroups.  Work item s is (query block, head) with the query
-  // blocks ordered by decreasing key count: s / nheads-th heaviest block of
-  // head s % nheads.  Round r gives item r * P + g to workgroup g on even
-  // rounds and r * P + P - 1 - g on odd ones (P workgroups), so that the
-  // heaviest and lightest blocks pair up and, with causal masking (key
-  // counts falling linearly with the block index), every workgroup gets the
-  // same number of key tiles.
+  // Persistent workgroups.  The work items (query block, query head) are
+  // numbered KV head first, then query block by decreasing key count, then
+  // query head within the KV head's group, so that neighbouring items read
+  // the same K and V.  Workgroup g runs on XCD g mod kXcds (the order in
+  // which the dispatcher hands out the first workgroups), and each XCD takes
+  // one contiguous share of the items, so the concurrent readers of a K/V
+  // tile share that XCD's L2.  Within an XCD, round r gives item r * Pl + c
+  // to the c-th of its Pl workgroups on even rounds and r * Pl + Pl - 1 - c on
+  // odd ones: heavy and light query blocks pair up, and with causal masking
+  // (key counts falling linearly with the block index) every workgroup gets
+  // the same number of key tiles.
   const int P = gridDim.x;
   const int wg = blockIdx.x;
+  const int X = p.nxcd;
+  const int xcd = wg % X, c = wg / X, Pl = P / X;
+  const int s0 = (int)((long long)p.nitems * xcd / X);
+  const int s1 = (int)((long long)p.nitems * (xcd + 1) / X);
+  const int per_kv = p.nqb * p.group;
   for (int round = 0;; ++round) {
-    const int s = round * P + ((round & 1) ? P - 1 - wg : wg);
-    if (s >= p.nitems) break;
-    const int head = s % p.nheads;
-    const int qb = p.nqb - 1 - s / p.nheads;
+    const int sl = round * Pl + ((round & 1) ? Pl - 1 - c : c);
+    if (sl >= s1 - s0) break;
+    const int s = s0 + sl;
+    const int kvh = s / per_kv;
+    const int rem = s - kvh * per_kv;
+    const int qb = p.nqb - 1 - rem / p.group;
+    const int head = kvh * p.group + rem % p.group;
     const int b = head / p.Hq;
     const int hq = head - b * p.Hq;
     const int hk = hq / p.group;
@@ -627,8 +647,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       st.alpha[rb] = 1.f;
     }
     const int rows = min(Lk, nt * BN);
-    auto copy_tile = [&](const T* base, uint32_t slot, int t) __attribute__((always_inline)) {
-      PF::copy_tile(base, slot, t, rows, wave, dof);
+    // Iteration j handles key tile tile(j).  With ALiBi the tiles are visited
+    // from the last to the first: the bias grows with the key index, so the
+    // first tile holds the largest bias of each row and the running maximum
+    // rarely grows afterwards (each growth beyond the lazy threshold costs a
+    // rescale of O^T).  Otherwise the keys run forward.
+    auto tile = [&](int j) __attribute__((always_inline)) { return REV ? nt - 1 - j : j; };
+    auto copy_tile = [&](const T* base, uint32_t slot, int j) __attribute__((always_inline)) {
+      PF::copy_tile(base, slot, tile(j), rows, wave, dof);
     };
 
     TileArgs ta;
@@ -637,9 +663,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     // Per-tile softmax parameters.  Tiles outside [0, n_w) are fully masked
     // (lim = -1): their softmax leaves the state unchanged and gives P = 0.
     auto set_tile = [&](int j) __attribute__((always_inline)) {
-      const int j0 = j * BN;
+      const int t = tile(j);
+      const int j0 = t * BN;
       ta.abase = ALIBI ? ta.sl2 * (float)(j0 + 4 * hh - iw - off) : 0.f;
-      const bool live = j >= 0 && j < n_w;
+      const bool live = t >= 0 && t < n_w;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         int l = Lk - 1 - j0 - 4 * hh;
@@ -650,8 +677,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 
     Scores sc[2];
     Probs pr[2];
-    // P of tile -2 is zero.  Pinned, so that the zeros are materialised in
-    // VGPRs here and not just before the first P.V MFMA that reads them.
+    // P of iteration -2 is zero (iteration -1 writes a zero P as well, and
+    // idle iterations leave both in place).  Pinned, so that the zeros are
+    // materialised in VGPRs here and not just before the first P.V MFMA that
+    // reads them.
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -663,18 +692,19 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
           pr[0].w[rb][c][w] = z;
         }
 
-    // Iteration j (from -1): copies of K_{j+kRing} and V_{j+kRing-2}; S^T of
-    // tile j+1, softmax of tile j, P.V of tile j-1, then the pending repair of
-    // O^T.  Tile t of K or V lives in slot t mod kRing: a copy is issued
-    // kRing - 1 iterations before the tile's first use, into the slot read by
-    // the iteration before, and waited for only at the end of the iteration
-    // before its use (vmcnt allows the copies of the last two iterations to
-    // be in flight; every iteration issues the same number of copies).  The
-    // scores and probabilities of tile j live in the register buffers of the
+    // Iteration j (from -1; "tile j" below is tile(j)): copies of K_{j+kRing}
+    // and V_{j+kRing-2}; S^T of tile j+1, softmax of tile j, P.V of tile j-1,
+    // then the pending repair of O^T.  The K or V tile of iteration j lives in
+    // slot j mod kRing: a copy is issued kRing - 1 iterations before the
+    // tile's first use, into the slot read by the iteration before, and
+    // waited for only at the end of the iteration before its use (vmcnt
+    // allows the copies of the last two iterations to be in flight; every
+    // iteration issues the same number of copies).  The scores and
+    // probabilities of iteration j live in the register buffers of the
     // parity of j.  VAR is 1 for tiles every row of the wave sees whole, 2 for
     // masked tiles (including the tiles outside [0, n_w), whose softmax is a
-    // no-op: P = 0, K unused), 0 for waves that have run out of tiles (copies
-    // and barrier only).
+    // no-op: P = 0, K unused), 0 for iterations in which the wave has no
+    // S^T, softmax or P.V to do (copies and barrier only).
     auto iteration = [&](int j, auto var, auto slotc) __attribute__((always_inline)) {
       constexpr int VAR = decltype(var)::value;
       constexpr int k = decltype(slotc)::value;   // j mod kRing
@@ -707,8 +737,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       }
     };
 
-    // Prologue: K_0 .. K_{kRing-2} and V_0 in flight, the V slots of tiles -1 and
-    // -2 zeroed (the first two iterations multiply them by P = 0).
+    // Prologue: the K tiles of iterations 0 .. kRing-2 and the V tile of
+    // iteration 0 in flight, the V slots of iterations -1 and -2 zeroed (the
+    // first two iterations multiply them by P = 0).
     {
       constexpr int NV16 = TE * (int)sizeof(T) / 16;
       uint4* vz = reinterpret_cast<uint4*>(lds + (kRing + kRing - 2) * TE);   // slots kRing-2, kRing-1
@@ -720,11 +751,24 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     copy_tile(vp, vslot(0), 0);
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
-    const int m0 = max(fm_w, 0);
-    iteration(-1, std::integral_constant<int, 2>{}, std::integral_constant<int, kRing - 1>{});
-    phase(0, fm_w, std::integral_constant<int, 1>{});
-    phase(m0, n_w + 1, std::integral_constant<int, 2>{});
-    phase(n_w + 1, nt + 1, std::integral_constant<int, 0>{});
+    const std::integral_constant<int, 0> idle;
+    const std::integral_constant<int, 1> whole;
+    const std::integral_constant<int, 2> masked;
+    iteration(-1, masked, std::integral_constant<int, kRing - 1>{});
+    if constexpr (REV) {
+      // Tiles [n_w + 1, nt) first (nothing to do), then n_w (its S^T of
+      // tile n_w - 1 is the first needed), the masked tiles [fm_w, n_w), the
+      // whole tiles, and the P.V of tile 0.
+      const int a = max(0, nt - n_w - 1);
+      phase(0, a, idle);
+      phase(a, nt - fm_w, masked);
+      phase(nt - fm_w, nt, whole);
+      phase(nt, nt + 1, masked);
+    } else {
+      phase(0, fm_w, whole);
+      phase(max(fm_w, 0), n_w + 1, masked);
+      phase(n_w + 1, nt + 1, idle);
+    }
 
     // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
     // head dims 32 db + 8 g + 4 hh + 0..3 of its row.  The scores of the last
@@ -778,6 +822,7 @@ hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
   q.nitems = p.nqb * q.nheads;
   if (q.nitems == 0) return hipSuccess;
   const int grid = std::min(q.nitems, compute_units());
+  q.nxcd = grid % kXcds == 0 ? kXcds : 1;
   hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI>), dim3(grid), dim3(kThreads), 0, stream, q);
   return hipGetLastError();
 }

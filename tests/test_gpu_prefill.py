@@ -1,6 +1,6 @@
 """GPU parity of the fused prefill kernel (attn_fwd) against the fp64 oracle.
 
-Small shapes span several 128-row query blocks and 64-key tiles with ragged
+Small shapes span several 256-row query blocks and 32-key tiles with ragged
 tails and are compared element by element; the full-size workloads run in the
 launch configuration the bench times and are compared on sampled rows the
 oracle computes one by one.
@@ -28,6 +28,11 @@ CASES = [  # B, Hq, Hkv, Lq, Lk, D, dtype, causal, alibi
     (1, 2, 2, 190, 64, 64, "f16", True, False),     # Lq > Lk: the first rows see no key
     (1, 2, 1, 1, 300, 128, "f16", True, False),     # a single query row
     (1, 3, 1, 65, 65, 64, "bf16", False, True),     # 3 query heads per KV head
+    (1, 4, 4, 700, 700, 64, "bf16", True, True),    # ALiBi: keys visited last to first, 3 query blocks
+    (1, 2, 2, 300, 777, 128, "f16", True, True),    # ALiBi causal with Lk > Lq
+    (1, 2, 2, 520, 300, 64, "f16", False, True),    # ALiBi without mask, Lq > Lk, ragged keys
+    (1, 2, 2, 530, 200, 128, "bf16", True, True),   # ALiBi causal, Lq > Lk: rows and waves with no key
+    (1, 2, 1, 600, 1000, 128, "bf16", False, False),
     (1, 4, 4, 130, 70, 128, "f16", False, False),
     (1, 2, 2, 1, 1, 64, "bf16", True, True),
     (1, 2, 2, 520, 520, 64, "f16", True, True),
