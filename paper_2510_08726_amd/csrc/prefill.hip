@@ -588,78 +588,121 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   const int s0 = (int)((long long)p.nitems * xcd / X);
   const int s1 = (int)((long long)p.nitems * (xcd + 1) / X);
   const int per_kv = p.nqb * p.group;
-  for (int round = 0;; ++round) {
-    const int sl = round * Pl + ((round & 1) ? Pl - 1 - c : c);
-    if (sl >= s1 - s0) break;
-    const int s = s0 + sl;
-    const int kvh = s / per_kv;
-    const int rem = s - kvh * per_kv;
-    const int qb = p.nqb - 1 - rem / p.group;
-    const int head = kvh * p.group + rem % p.group;
-    const int b = head / p.Hq;
-    const int hq = head - b * p.Hq;
-    const int hk = hq / p.group;
-    const int Lq = p.Lq, Lk = p.Lk;
-    const int off = Lk - Lq;
-    const int i0 = qb * BM;
-    const int iw = i0 + BMW * wave;   // first row of this wave
-    const int row0 = iw + n;          // this lane's row in row block 0
+  const int Lq = p.Lq, Lk = p.Lk;
+  const int off = Lk - Lq;
 
-    // Tiles: the workgroup stages [0, nt); this wave computes [0, n_w); tiles
-    // [0, fm_w) need no mask for any of its rows.
+  // One work item: its query block and head, and the key tiles [0, nt) that
+  // the workgroup stages, [0, n_w) that this wave computes and [0, fm_w) that
+  // no row of this wave masks.
+  struct Item {
+    int qb, head, kvh, hq, iw, nt, n_w, fm_w, rows;
+  };
+  auto item_at = [&](int round, Item& it) __attribute__((always_inline)) {
+    const int sl = round * Pl + ((round & 1) ? Pl - 1 - c : c);
+    if (sl >= s1 - s0) return false;
+    const int s = s0 + sl;
+    it.kvh = s / per_kv;
+    const int rem = s - it.kvh * per_kv;
+    it.qb = p.nqb - 1 - rem / p.group;
+    it.head = it.kvh * p.group + rem % p.group;
+    it.hq = it.head % p.Hq;
+    const int i0 = it.qb * BM;
+    it.iw = i0 + BMW * wave;
     int kend = Lk, kend_w = Lk;
     if (CAUSAL) {
       kend = min(Lk, min(i0 + BM, Lq) + off);
-      kend_w = min(Lk, min(iw + BMW, Lq) + off);
+      kend_w = min(Lk, min(it.iw + BMW, Lq) + off);
     }
-    if (iw >= Lq) kend_w = 0;
-    const int nt = kend > 0 ? (kend + BN - 1) / BN : 0;
-    const int n_w = kend_w > 0 ? (kend_w + BN - 1) / BN : 0;
-    int fm_w = Lk / BN;
-    if (CAUSAL) fm_w = min(fm_w, max(0, (iw + off + 1) / BN));
-    fm_w = min(fm_w, n_w);
+    if (it.iw >= Lq) kend_w = 0;
+    it.nt = kend > 0 ? (kend + BN - 1) / BN : 0;
+    it.n_w = kend_w > 0 ? (kend_w + BN - 1) / BN : 0;
+    int fm = Lk / BN;
+    if (CAUSAL) fm = min(fm, max(0, (it.iw + off + 1) / BN));
+    it.fm_w = min(fm, it.n_w);
+    it.rows = min(Lk, it.nt * BN);
+    return true;
+  };
+  auto kbase = [&](const Item& it) __attribute__((always_inline)) {
+    return reinterpret_cast<const T*>(p.k) + (size_t)it.kvh * Lk * D;
+  };
+  auto vbase = [&](const Item& it) __attribute__((always_inline)) {
+    return reinterpret_cast<const T*>(p.v) + (size_t)it.kvh * Lk * D;
+  };
+  // Iteration j handles key tile tile(j).  With ALiBi the tiles are visited
+  // from the last to the first: the bias grows with the key index, so the
+  // first tile holds the largest bias of each row and the running maximum
+  // rarely grows afterwards (each growth beyond the lazy threshold costs a
+  // rescale of O^T).  Otherwise the keys run forward.
+  auto tile_of = [&](const Item& it, int j) __attribute__((always_inline)) { return REV ? it.nt - 1 - j : j; };
 
-    const T* qp = reinterpret_cast<const T*>(p.q) + (size_t)head * Lq * D;
-    const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)(b * p.Hkv + hk) * Lk * D;
-    const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)(b * p.Hkv + hk) * Lk * D;
+  // Start of an item: the V slots of iterations -1 and -2 zeroed (the first
+  // two iterations multiply them by P = 0), the copies of the K tiles of
+  // iterations 0 .. kRing-2 and of the V tile of iteration 0 issued, and this
+  // lane's Q fragments (B operand of S^T: lane (n, hh) holds
+  // Q[row][16 kx + 8 hh + 0..7]) loaded into qv.  It runs while the previous
+  // item's output is still being written, after the barrier that ends the
+  // previous item's last LDS reads; the caller waits for all of it.
+  u32x4 qv[RB * KX];
+  auto start_item = [&](const Item& it) __attribute__((always_inline)) {
+    {
+      constexpr int NV16 = TE * (int)sizeof(T) / 16;
+      uint4* vz = reinterpret_cast<uint4*>(lds + (kRing + kRing - 2) * TE);   // slots kRing-2, kRing-1
+#pragma unroll
+      for (int i = tid; i < 2 * NV16; i += kThreads) vz[i] = make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kRing - 1; ++j) PF::copy_tile(kbase(it), kslot(j), tile_of(it, j), it.rows, wave, dof);
+    PF::copy_tile(vbase(it), vslot(0), tile_of(it, 0), it.rows, wave, dof);
+    const T* qp = reinterpret_cast<const T*>(p.q) + (size_t)it.head * Lq * D;
+#pragma unroll
+    for (int f = 0; f < RB * KX; ++f) {
+      const int rb = f / KX, kx = f % KX;
+      const int row = it.iw + n + 32 * rb;
+      u32x4 w = {0u, 0u, 0u, 0u};
+      if (row < Lq) w = *reinterpret_cast<const u32x4*>(qp + (size_t)row * D + 16 * kx + 8 * hh);
+      qv[f] = w;
+    }
+  };
 
-    State st;
-    // Q fragments (B operand of S^T): lane (n, hh) holds Q[row][16 kx + 8 hh + 0..7],
-    // written once into their AGPRs; O^T starts at zero.
+  Item cur;
+  if (!item_at(0, cur)) return;
+  start_item(cur);
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  agpr_write<kOnesAgpr>(PF::M::kOnes);
+  agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
+
+  for (int round = 0;; ++round) {
+    const int nt = cur.nt, n_w = cur.n_w, fm_w = cur.fm_w;
+    const int iw = cur.iw;
+    const int row0 = iw + n;          // this lane's row in row block 0
+    const T* kp = kbase(cur);
+    const T* vp = vbase(cur);
+
+    // Q into its AGPRs (negated for a negative scale); O^T and l start at zero.
     static_for<RB * KX>([&](auto ic) {
       constexpr int f = decltype(ic)::value;
       constexpr int rb = f / KX, kx = f % KX;
-      const int row = row0 + 32 * rb;
-      uint4 w = make_uint4(0, 0, 0, 0);
-      if (row < Lq) w = *reinterpret_cast<const uint4*>(qp + (size_t)row * D + 16 * kx + 8 * hh);
-      agpr_write<PF::qagpr(rb, kx) + 0>(w.x ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 1>(w.y ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 2>(w.z ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 3>(w.w ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 0>(qv[f][0] ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 1>(qv[f][1] ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 2>(qv[f][2] ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 3>(qv[f][3] ^ p.qsign);
     });
     static_for<RB * PF::DB * 16>([&](auto ic) { agpr_zero<decltype(ic)::value>(); });
     static_for<RB * 4>([&](auto ic) { agpr_zero<kLAgpr + decltype(ic)::value>(); });
-    agpr_write<kOnesAgpr>(PF::M::kOnes);
-    agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
+    State st;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       st.mc[rb] = kMcInit;
       st.alpha[rb] = 1.f;
     }
-    const int rows = min(Lk, nt * BN);
-    // Iteration j handles key tile tile(j).  With ALiBi the tiles are visited
-    // from the last to the first: the bias grows with the key index, so the
-    // first tile holds the largest bias of each row and the running maximum
-    // rarely grows afterwards (each growth beyond the lazy threshold costs a
-    // rescale of O^T).  Otherwise the keys run forward.
-    auto tile = [&](int j) __attribute__((always_inline)) { return REV ? nt - 1 - j : j; };
+    auto tile = [&](int j) __attribute__((always_inline)) { return tile_of(cur, j); };
     auto copy_tile = [&](const T* base, uint32_t slot, int j) __attribute__((always_inline)) {
-      PF::copy_tile(base, slot, tile(j), rows, wave, dof);
+      PF::copy_tile(base, slot, tile(j), cur.rows, wave, dof);
     };
 
     TileArgs ta;
     ta.c = p.c;
-    ta.sl2 = ALIBI ? p.slopes[hq] * kLog2e : 0.f;
+    ta.sl2 = ALIBI ? p.slopes[cur.hq] * kLog2e : 0.f;
     // Per-tile softmax parameters.  Tiles outside [0, n_w) are fully masked
     // (lim = -1): their softmax leaves the state unchanged and gives P = 0.
     auto set_tile = [&](int j) __attribute__((always_inline)) {
@@ -684,12 +727,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
           uint32_t z = 0u;
           pin(z);
-          pr[0].w[rb][c][w] = z;
+          pr[0].w[rb][cc][w] = z;
         }
 
     // Iteration j (from -1; "tile j" below is tile(j)): copies of K_{j+kRing}
@@ -737,20 +780,6 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       }
     };
 
-    // Prologue: the K tiles of iterations 0 .. kRing-2 and the V tile of
-    // iteration 0 in flight, the V slots of iterations -1 and -2 zeroed (the
-    // first two iterations multiply them by P = 0).
-    {
-      constexpr int NV16 = TE * (int)sizeof(T) / 16;
-      uint4* vz = reinterpret_cast<uint4*>(lds + (kRing + kRing - 2) * TE);   // slots kRing-2, kRing-1
-#pragma unroll
-      for (int i = tid; i < 2 * NV16; i += kThreads) vz[i] = make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int t = 0; t < kRing - 1; ++t) copy_tile(kp, kslot(t), t);
-    copy_tile(vp, vslot(0), 0);
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-
     const std::integral_constant<int, 0> idle;
     const std::integral_constant<int, 1> whole;
     const std::integral_constant<int, 2> masked;
@@ -769,6 +798,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       phase(max(fm_w, 0), n_w + 1, masked);
       phase(n_w + 1, nt + 1, idle);
     }
+
+    // The next item's copies and Q loads go out before this item's output is
+    // written, so that their latencies overlap.
+    Item nxt;
+    const bool more = item_at(round + 1, nxt);
+    if (more) start_item(nxt);
 
     // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
     // head dims 32 db + 8 g + 4 hh + 0..3 of its row.  The scores of the last
@@ -795,10 +830,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       w.y = PF::E::pack2(agpr_read<a0 + 2>() * inv, agpr_read<a0 + 3>() * inv);
       const int row = row0 + 32 * rb;
       if (row < Lq) {
-        T* op = reinterpret_cast<T*>(p.o) + ((size_t)head * Lq + row) * D;
+        T* op = reinterpret_cast<T*>(p.o) + ((size_t)cur.head * Lq + row) * D;
         *reinterpret_cast<uint2*>(op + 32 * db + 8 * g + 4 * hh) = w;
       }
     });
+    if (!more) break;
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    cur = nxt;
   }
 }
 
