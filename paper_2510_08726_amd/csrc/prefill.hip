@@ -446,40 +446,52 @@ struct Prefill {
     }
   }
 
+  // Fragment i of an iteration: group i / 2, the K fragment of the group
+  // first, then its V fragment.  Fragment i lives in ring entry i mod
+  // (PFD + 1) and is read PFD fragments ahead of its MFMAs; the first PFD
+  // fragments of an iteration are read at the end of the iteration before.
+  static constexpr int NF = 2 * NG;   // fragments per iteration
+  static_assert(NF % (PFD + 1) == 0, "fragment ring positions must repeat every iteration");
+  // LDS instructions that read the first PFD fragments (a K fragment takes
+  // one, a V fragment two).
+  static constexpr int kPrimeReads = (PFD + 1) / 2 + 2 * (PFD / 2);
+  typedef vec8 Ring[PFD + 1];
+
+  template <int I>
+  static __device__ __forceinline__ void read_frag(Ring& fr, const T* kl, const T* vl, const Addr& ad) {
+    if constexpr (I % 2 == 0) fr[I % (PFD + 1)] = kfrag(kl, ad, I / 2);
+    else fr[I % (PFD + 1)] = vfrag(vl, ad, I / 2);
+  }
+  // The first PFD fragments of the iteration whose tiles are kl and vl.
+  static __device__ __forceinline__ void prime(Ring& fr, const T* kl, const T* vl, const Addr& ad) {
+    static_for<PFD>([&](auto ic) { read_frag<decltype(ic)::value>(fr, kl, vl, ad); });
+  }
+
   // One iteration of the software pipeline: S^T of tile j+1 (QK), softmax of
-  // tile j (SM: 0 none, 1 unmasked, 2 masked), P.V of tile j-1 (PV).  Group g
-  // holds the slots [QK rb 0, QK rb 1, PV rb 0, PV rb 1] of K fragment g and V
-  // fragment g (the parts present); each fragment is read from LDS PFD
-  // fragments ahead of its first slot.
+  // tile j (SM: 1 unmasked, 2 masked), P.V of tile j-1 (PV).  Group g holds
+  // the slots [QK rb 0, QK rb 1, PV rb 0, PV rb 1] of K fragment g and V
+  // fragment g.  kl, vl are this iteration's K and V tiles, kln, vln the next
+  // iteration's (its first fragments are read in the last slots).
+
   template <bool QK, int SM, bool PV>
   static __device__ __forceinline__ bool iterate(State& st, Scores& s_cur, Scores& s_next, Probs& p_cur,
-                                                 const Probs& p_prev, const T* kl, const T* vl, const Addr& ad,
-                                                 const TileArgs& ta) {
+                                                 const Probs& p_prev, Ring& fr, const T* kl, const T* vl,
+                                                 const T* kln, const T* vln, const Addr& ad, const TileArgs& ta) {
+    static_assert(QK && PV, "every iteration issues both products");
     constexpr bool MASKED = SM == 2;
     constexpr bool PREP = ALIBI || MASKED;
     typedef SoftPlan<PREP, MASKED, ALIBI> P;
-    constexpr int FPG = (QK ? 1 : 0) + (PV ? 1 : 0);   // fragments per group
-    constexpr int NF = NG * FPG;                        // fragments of the iteration
-    constexpr int NS = 2 * NF;                          // MFMA slots
+    constexpr int FPG = 2;        // fragments per group
+    constexpr int NS = 2 * NF;    // MFMA slots
     Tmp tp;
     tp.rep = 0;
-    vec8 fr[PFD + 1];
-    // Fragment i of the iteration: group i / FPG, K first when both.
+    // Fragments NF .. NF + PFD - 1 are the first ones of the next iteration.
     auto read = [&](auto ic) {
       constexpr int i = decltype(ic)::value;
-      if constexpr (i < NF) {
-        constexpr int g = i / FPG;
-        constexpr bool is_k = QK && (i % FPG == 0);
-        if constexpr (is_k) fr[i % (PFD + 1)] = kfrag(kl, ad, g);
-        else fr[i % (PFD + 1)] = vfrag(vl, ad, g);
-      }
+      if constexpr (i < NF) read_frag<i>(fr, kl, vl, ad);
+      else read_frag<i - NF>(fr, kln, vln, ad);
     };
-    if constexpr (NS == 0) {
-      if constexpr (SM != 0) soft_range<0, P::NSTEP, PREP, MASKED>(st, s_cur, p_cur, tp, ta);
-    } else {
-      [&]<int... Is>(std::integer_sequence<int, Is...>) {
-        (read(std::integral_constant<int, Is>{}), ...);
-      }(std::make_integer_sequence<int, PFD>{});
+    {
       [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
         (
             [&] {
@@ -720,6 +732,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 
     Scores sc[2];
     Probs pr[2];
+    typename PF::Ring fr;
     // P of iteration -2 is zero (iteration -1 writes a zero P as well, and
     // idle iterations leave both in place).  Pinned, so that the zeros are
     // materialised in VGPRs here and not just before the first P.V MFMA that
@@ -738,34 +751,43 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     // Iteration j (from -1; "tile j" below is tile(j)): copies of K_{j+kRing}
     // and V_{j+kRing-2}; S^T of tile j+1, softmax of tile j, P.V of tile j-1,
     // then the pending repair of O^T.  The K or V tile of iteration j lives in
-    // slot j mod kRing: a copy is issued kRing - 1 iterations before the
-    // tile's first use, into the slot read by the iteration before, and
-    // waited for only at the end of the iteration before its use (vmcnt
-    // allows the copies of the last two iterations to be in flight; every
-    // iteration issues the same number of copies).  The scores and
-    // probabilities of iteration j live in the register buffers of the
-    // parity of j.  VAR is 1 for tiles every row of the wave sees whole, 2 for
-    // masked tiles (including the tiles outside [0, n_w), whose softmax is a
-    // no-op: P = 0, K unused), 0 for iterations in which the wave has no
-    // S^T, softmax or P.V to do (copies and barrier only).
+    // slot j mod kRing.  A tile's first fragments are read at the end of the
+    // iteration before its use, so its copy, issued kRing - 1 iterations
+    // before its use into the slot read by the iteration before, must be
+    // complete at the barrier that ends the iteration two before its use:
+    // vmcnt lets only the current iteration's copies stay in flight (every
+    // iteration issues the same number of copies), and lgkmcnt lets the reads
+    // of the next iteration's first fragments, which touch neither slot
+    // copied into next, cross the barrier.  The scores and probabilities of
+    // iteration j live in the register buffers of the parity of j.  VAR is 1
+    // for tiles every row of the wave sees whole, 2 for masked tiles
+    // (including the tiles outside [0, n_w), whose softmax is a no-op: P = 0,
+    // K unused), 0 for iterations in which the wave has no S^T, softmax or
+    // P.V to do (copies, the next iteration's first fragments and the
+    // barrier only).
     auto iteration = [&](int j, auto var, auto slotc) __attribute__((always_inline)) {
       constexpr int VAR = decltype(var)::value;
       constexpr int k = decltype(slotc)::value;   // j mod kRing
       constexpr int par = k & 1;
       copy_tile(kp, kslot(k), j + kRing);
       copy_tile(vp, vslot((k + kRing - 2) % kRing), j + kRing - 2);
+      const T* kl_nxt = lds + ((k + 2) % kRing) * TE;   // K_{j+2}
+      const T* vl_nxt = lds + (kRing + k) * TE;         // V_j
       if constexpr (VAR != 0) {
         set_tile(j);
         const T* kl_use = lds + ((k + 1) % kRing) * TE;                  // K_{j+1}
         const T* vl_use = lds + (kRing + (k + kRing - 1) % kRing) * TE;  // V_{j-1}
-        const bool rep = PF::template iterate<true, VAR, true>(st, sc[par], sc[par ^ 1], pr[par], pr[par ^ 1], kl_use,
-                                                               vl_use, ad, ta);
+        const bool rep = PF::template iterate<true, VAR, true>(st, sc[par], sc[par ^ 1], pr[par], pr[par ^ 1], fr,
+                                                               kl_use, vl_use, kl_nxt, vl_nxt, ad, ta);
         if (__builtin_amdgcn_ballot_w64(rep) != 0) PF::repair(st);
+      } else {
+        PF::prime(fr, kl_nxt, vl_nxt, ad);
       }
       // 16 wait states between this iteration's last MFMAs and the next
-      // iteration's first reads of their results; the copies of all but the
-      // last two iterations complete; then the barrier publishes them.
-      asm volatile("s_nop 7\n\ts_nop 7\n\ts_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(4 * NI) : "memory");
+      // iteration's first reads of their results, the waits described above,
+      // then the barrier that publishes the completed copies.
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_waitcnt vmcnt(%0) lgkmcnt(%1)\n\ts_barrier"
+                   : : "n"(2 * NI), "n"(PF::kPrimeReads) : "memory");
     };
     // Iterations j in [j0, j1), j0 >= 0, of one variant; the loop body is
     // unrolled by kRing so that slots and parities are compile-time choices.
@@ -783,6 +805,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     const std::integral_constant<int, 0> idle;
     const std::integral_constant<int, 1> whole;
     const std::integral_constant<int, 2> masked;
+    // The first fragments of iteration -1: K_0 and the zeroed V slot.
+    PF::prime(fr, lds, lds + (kRing + kRing - 2) * TE, ad);
     iteration(-1, masked, std::integral_constant<int, kRing - 1>{});
     if constexpr (REV) {
       // Tiles [n_w + 1, nt) first (nothing to do), then n_w (its S^T of
