@@ -76,15 +76,16 @@ constexpr int BM = BMW * kWaves;            // query rows per workgroup
 constexpr int BN = 32;                      // keys per tile
 constexpr int PFD = 3;                      // operand fragments read ahead
 constexpr int kRing = 4;                    // LDS slots per operand; copies run kRing - 1 tiles ahead
-constexpr float kLazyThreshold = 8.f;       // log2 units
+// A row's reference maximum moves only when a tile's maximum exceeds it by
+// more than this (log2 units), so that P <= 2^kLazyThreshold.
+constexpr float kLazyThreshold = 8.f;
 // Reference max (times c) before the first visible key: finite, so the first
-// tile's decision and repair factor need no special case (its repair factor
-// underflows to 0, and O^T and l are still 0 then).
+// visible tile takes the slow path like any other move and its rescale factor
+// underflows to 0 (O^T and l are still 0 then).
+constexpr float kMcInit = -1e30f;
 // Accelerator dies (XCDs), each with its own L2; consecutive workgroups of a
 // launch are dealt to them in turn.
 constexpr int kXcds = 8;
-constexpr float kMcInit = -1e30f;
-constexpr float kMcFresh = -1e29f;
 
 // K and V tiles live in LDS row-major, [BN][D], with the 16-byte chunks of
 // each row XOR-swizzled: chunk c of row r sits at chunk position c ^ swz(r).
@@ -243,15 +244,17 @@ __device__ __forceinline__ void static_for(F&& f) {
 // (the exp-sum is accumulated by rowsum MFMAs beside P.V).
 template <bool PREP, bool MASKED, bool ALIBI>
 struct SoftPlan {
+  // Steps [0, MAX0) prepare the scores (ALiBi bias, mask), four registers a
+  // step; then come 16 exponential steps (two registers each) and 8 steps of
+  // the lane's running maximum (four registers each), as exp, exp, max.
   static constexpr int MAX0 = PREP ? 4 : 0;
-  static constexpr int FIN0 = MAX0 + 8;
-  static constexpr int EXP0 = FIN0 + 1;
-  static constexpr int NSTEP = EXP0 + 16;
+  static constexpr int NSTEP = MAX0 + 24;
+  static constexpr bool is_exp(int k) { return k >= MAX0 && (k - MAX0) % 3 != 2; }
+  static constexpr int exp_index(int k) { return 2 * ((k - MAX0) / 3) + (k - MAX0) % 3; }
+  static constexpr int max_index(int k) { return (k - MAX0) / 3; }
   static constexpr int weight(int k) {
     if (k < MAX0) return (ALIBI ? 12 : 0) * 4 + (MASKED ? 16 : 0) * 4;
-    if (k < FIN0) return 8;
-    if (k < EXP0) return 80;
-    return 30;
+    return is_exp(k) ? 30 : 8;
   }
   // First step of slot s when the steps are spread over ns slots.
   static constexpr int begin(int s, int ns) {
@@ -291,7 +294,7 @@ struct Prefill {
   };
   struct State {
     float mc[RB];     // reference max of the row, times ce (log2 units)
-    float alpha[RB];  // pending repair factor of O^T and l
+    float alpha[RB];  // rescale factor of O^T and l set by the slow path
   };
   static constexpr int oagpr(int rb, int db) { return 16 * (rb * DB + db); }
   static constexpr int qagpr(int rb, int kx) { return kQAgpr + 4 * (rb * KX + kx); }
@@ -303,8 +306,7 @@ struct Prefill {
   };
   // Softmax scratch of one tile.
   struct Tmp {
-    float t[RB];
-    uint32_t rep;     // nonzero: some row of this lane needs O^T repaired
+    float t[RB];      // this lane's maximum score of the tile, per row block
   };
   struct TileArgs {
     float c;      // scale * log2(e) (with ALiBi) or max(|scale| * log2(e), tiny)
@@ -333,6 +335,26 @@ struct Prefill {
     for (int u = 0; u < NI; ++u)
       asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                    : : "s"(slot + (uint32_t)((u * kWaves + wave) * 1024)), "v"(dof[u]), "s"(rsrc) : "memory", "m0");
+  }
+
+  // This wave's copy of the RB * 32 rows at `base` into its LDS region at
+  // byte address `dst`, in the layout of a K tile (row r at r * D elements,
+  // chunk c at chunk position c ^ swz(r)); rows at or past `left` read as
+  // zero.  Only the copying wave reads the region.
+  static __device__ __forceinline__ void copy_rows(const T* base, uint32_t dst, int left, int lane) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const int nb = max(min(left, RB * 32), 0) * D * (int)sizeof(T);
+    const u32x4 rsrc = {(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
+                        (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
+                        (uint32_t)__builtin_amdgcn_readfirstlane(nb), 0x00020000u};
+#pragma unroll
+    for (int blk = 0; blk < RB * TE * (int)sizeof(T) / 1024; ++blk) {
+      const int r = blk * (1024 / (2 * D)) + lane / CPR;
+      const int pos = lane % CPR;
+      const int goff = (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T);
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                   : : "s"(dst + (uint32_t)(blk * 1024)), "v"(goff), "s"(rsrc) : "memory", "m0");
+    }
   }
 
   static __device__ __forceinline__ void make_addr(Addr& ad, int lane) {
@@ -403,38 +425,61 @@ struct Prefill {
           sc.s[rb][r] = x;
         }
       }
-    } else if constexpr (K < P::FIN0) {
-      constexpr int k = K - P::MAX0;
-      constexpr int q = k / 2, rb = k % 2;
-      const f32x16& s = sc.s[rb];
-      const float m4 = fmaxf(fmaxf(s[4 * q], s[4 * q + 1]), fmaxf(s[4 * q + 2], s[4 * q + 3]));
-      if constexpr (q == 0) tp.t[rb] = m4;
-      else tp.t[rb] = fmaxf(tp.t[rb], m4);
-      pin(tp.t[rb]);
-    } else if constexpr (K < P::EXP0) {
-      float t0 = tp.t[0], t1 = tp.t[1];
-      max_halves2(t0, t1);
-      const float tm[RB] = {t0, t1};
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const float d = __builtin_fmaf(tm[rb], ce, -st.mc[rb]);   // how far the tile max is above the reference
-        const bool move = d > kLazyThreshold;
-        tp.rep |= (move && st.mc[rb] > kMcFresh) ? 1u : 0u;
-        st.alpha[rb] = move ? fast_exp2(-d) : 1.f;
-        st.mc[rb] = move ? tm[rb] * ce : st.mc[rb];
-        pin(st.alpha[rb]);
-        pin(st.mc[rb]);
-      }
-      pin(tp.rep);
-    } else {
-      constexpr int k = K - P::EXP0;
+    } else if constexpr (P::is_exp(K)) {
+      constexpr int k = P::exp_index(K);
       constexpr int rb = k % 2, r = 2 * (k / 2);
       const float p0 = fast_exp2(__builtin_fmaf(sc.s[rb][r], ce, -st.mc[rb]));
       const float p1 = fast_exp2(__builtin_fmaf(sc.s[rb][r + 1], ce, -st.mc[rb]));
       uint32_t w = E::pack2(p0, p1);
       pin(w);
       pr.w[rb][r / 8][(r % 8) / 2] = w;
+    } else {
+      constexpr int k = P::max_index(K);
+      constexpr int q = k / 2, rb = k % 2;
+      const f32x16& s = sc.s[rb];
+      const float m4 = fmaxf(fmaxf(s[4 * q], s[4 * q + 1]), fmaxf(s[4 * q + 2], s[4 * q + 3]));
+      if constexpr (q == 0) tp.t[rb] = m4;
+      else tp.t[rb] = fmaxf(tp.t[rb], m4);
+      pin(tp.t[rb]);
     }
+  }
+
+  // After the steps of a tile: does some score of this lane exceed the
+  // reference maximum by more than the lazy threshold?  (Then the tile's P,
+  // computed against the old reference, must be recomputed: see resolve.)
+  static __device__ __forceinline__ bool exceeds(const State& st, const Tmp& tp, const TileArgs& ta) {
+    const float ce = ALIBI ? 1.f : ta.c;
+    bool x = false;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) x |= __builtin_fmaf(tp.t[rb], ce, -st.mc[rb]) > kLazyThreshold;
+    return x;
+  }
+
+  // Slow path of a tile whose maximum moved past the threshold in some row
+  // of the wave (always the case for a row's first visible tile, whose
+  // reference is still kMcInit): the row maximum is combined over the lane
+  // pair holding the row, rows that moved take it as their new reference,
+  // O^T and l are rescaled by 2^-(move) (the P.V products so far used the
+  // old reference), and the tile's P is recomputed.  Rows that did not move
+  // keep their reference and factor 1.
+  static __device__ __forceinline__ void resolve(State& st, Scores& sc, Probs& pr, Tmp& tp, const TileArgs& ta) {
+    typedef SoftPlan<false, false, ALIBI> P;
+    const float ce = ALIBI ? 1.f : ta.c;
+    float t0 = tp.t[0], t1 = tp.t[1];
+    max_halves2(t0, t1);
+    const float tm[RB] = {t0, t1};
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const float d = __builtin_fmaf(tm[rb], ce, -st.mc[rb]);
+      const bool move = d > kLazyThreshold;
+      st.alpha[rb] = move ? fast_exp2(-d) : 1.f;
+      st.mc[rb] = move ? tm[rb] * ce : st.mc[rb];
+    }
+    repair(st);
+    static_for<P::NSTEP>([&](auto kc) {
+      constexpr int K = decltype(kc)::value;
+      if constexpr (P::is_exp(K)) soft_step<K, false, false>(st, sc, pr, tp, ta);
+    });
   }
 
   template <int B0, int B1, bool PREP, bool MASKED>
@@ -476,15 +521,14 @@ struct Prefill {
   template <bool QK, int SM, bool PV>
   static __device__ __forceinline__ bool iterate(State& st, Scores& s_cur, Scores& s_next, Probs& p_cur,
                                                  const Probs& p_prev, Ring& fr, const T* kl, const T* vl,
-                                                 const T* kln, const T* vln, const Addr& ad, const TileArgs& ta) {
+                                                 const T* kln, const T* vln, const Addr& ad, const TileArgs& ta,
+                                                 Tmp& tp) {
     static_assert(QK && PV, "every iteration issues both products");
     constexpr bool MASKED = SM == 2;
     constexpr bool PREP = ALIBI || MASKED;
     typedef SoftPlan<PREP, MASKED, ALIBI> P;
     constexpr int FPG = 2;        // fragments per group
     constexpr int NS = 2 * NF;    // MFMA slots
-    Tmp tp;
-    tp.rep = 0;
     // Fragments NF .. NF + PFD - 1 are the first ones of the next iteration.
     auto read = [&](auto ic) {
       constexpr int i = decltype(ic)::value;
@@ -520,7 +564,7 @@ struct Prefill {
             ...);
       }(std::make_integer_sequence<int, NS>{});
     }
-    return tp.rep != 0;
+    return exceeds(st, tp, ta);
   }
 
   // O^T *= alpha and l *= alpha, in place in the AGPRs.
@@ -552,8 +596,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   constexpr int TE = PF::TE;
   constexpr int NI = PF::NI;
   constexpr int CPR = PF::CPR;
-  // LDS: a ring of kRing K tiles, then a ring of kRing V tiles.
-  __shared__ __attribute__((aligned(1024))) T lds[2 * kRing * TE];
+  // LDS: a ring of kRing K tiles, a ring of kRing V tiles, then one region
+  // of RB * 32 rows per wave that stages its Q block in and its O block out.
+  __shared__ __attribute__((aligned(1024))) T lds[2 * kRing * TE + kWaves * RB * TE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -648,13 +693,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   auto tile_of = [&](const Item& it, int j) __attribute__((always_inline)) { return REV ? it.nt - 1 - j : j; };
 
   // Start of an item: the V slots of iterations -1 and -2 zeroed (the first
-  // two iterations multiply them by P = 0), the copies of the K tiles of
-  // iterations 0 .. kRing-2 and of the V tile of iteration 0 issued, and this
-  // lane's Q fragments (B operand of S^T: lane (n, hh) holds
-  // Q[row][16 kx + 8 hh + 0..7]) loaded into qv.  It runs while the previous
-  // item's output is still being written, after the barrier that ends the
-  // previous item's last LDS reads; the caller waits for all of it.
-  u32x4 qv[RB * KX];
+  // two iterations multiply them by P = 0) and the copies of the K tiles of
+  // iterations 0 .. kRing-2 and of the V tile of iteration 0 issued.  It runs
+  // after the barrier that ends the previous item's last LDS reads, while the
+  // previous item's output is still being written; the caller waits for it.
   auto start_item = [&](const Item& it) __attribute__((always_inline)) {
     {
       constexpr int NV16 = TE * (int)sizeof(T) / 16;
@@ -665,20 +707,19 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 #pragma unroll
     for (int j = 0; j < kRing - 1; ++j) PF::copy_tile(kbase(it), kslot(j), tile_of(it, j), it.rows, wave, dof);
     PF::copy_tile(vbase(it), vslot(0), tile_of(it, 0), it.rows, wave, dof);
-    const T* qp = reinterpret_cast<const T*>(p.q) + (size_t)it.head * Lq * D;
-#pragma unroll
-    for (int f = 0; f < RB * KX; ++f) {
-      const int rb = f / KX, kx = f % KX;
-      const int row = it.iw + n + 32 * rb;
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (row < Lq) w = *reinterpret_cast<const u32x4*>(qp + (size_t)row * D + 16 * kx + 8 * hh);
-      qv[f] = w;
-    }
+  };
+  // This wave's staging region (Q rows in, O rows out) and the copy of an
+  // item's Q rows into it; the region's previous contents must have been read.
+  T* const qo = lds + 2 * kRing * TE + wave * RB * TE;
+  const uint32_t qo_addr = (uint32_t)(uintptr_t)(lds_void*)qo;
+  auto copy_q = [&](const Item& it) __attribute__((always_inline)) {
+    PF::copy_rows(reinterpret_cast<const T*>(p.q) + ((size_t)it.head * Lq + it.iw) * D, qo_addr, Lq - it.iw, lane);
   };
 
   Item cur;
   if (!item_at(0, cur)) return;
   start_item(cur);
+  copy_q(cur);
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   agpr_write<kOnesAgpr>(PF::M::kOnes);
   agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
@@ -690,14 +731,17 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     const T* kp = kbase(cur);
     const T* vp = vbase(cur);
 
-    // Q into its AGPRs (negated for a negative scale); O^T and l start at zero.
+    // Q fragments (B operand of S^T: lane (n, hh) holds Q[row][16 kx + 8 hh
+    // + 0..7], read like K fragments) into their AGPRs, negated for a
+    // negative scale; O^T and l start at zero.
     static_for<RB * KX>([&](auto ic) {
       constexpr int f = decltype(ic)::value;
       constexpr int rb = f / KX, kx = f % KX;
-      agpr_write<PF::qagpr(rb, kx) + 0>(qv[f][0] ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 1>(qv[f][1] ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 2>(qv[f][2] ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 3>(qv[f][3] ^ p.qsign);
+      const u32x4 w = __builtin_bit_cast(u32x4, PF::kfrag(qo + rb * TE, ad, kx));
+      agpr_write<PF::qagpr(rb, kx) + 0>(w[0] ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 1>(w[1] ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 2>(w[2] ^ p.qsign);
+      agpr_write<PF::qagpr(rb, kx) + 3>(w[3] ^ p.qsign);
     });
     static_for<RB * PF::DB * 16>([&](auto ic) { agpr_zero<decltype(ic)::value>(); });
     static_for<RB * 4>([&](auto ic) { agpr_zero<kLAgpr + decltype(ic)::value>(); });
@@ -750,7 +794,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 
     // Iteration j (from -1; "tile j" below is tile(j)): copies of K_{j+kRing}
     // and V_{j+kRing-2}; S^T of tile j+1, softmax of tile j, P.V of tile j-1,
-    // then the pending repair of O^T.  The K or V tile of iteration j lives in
+    // then, if tile j's maximum moved past the threshold in some row of the
+    // wave, the slow path (rescale of O^T and l, P recomputed).  The K or V tile of iteration j lives in
     // slot j mod kRing.  A tile's first fragments are read at the end of the
     // iteration before its use, so its copy, issued kRing - 1 iterations
     // before its use into the slot read by the iteration before, must be
@@ -777,9 +822,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
         set_tile(j);
         const T* kl_use = lds + ((k + 1) % kRing) * TE;                  // K_{j+1}
         const T* vl_use = lds + (kRing + (k + kRing - 1) % kRing) * TE;  // V_{j-1}
-        const bool rep = PF::template iterate<true, VAR, true>(st, sc[par], sc[par ^ 1], pr[par], pr[par ^ 1], fr,
-                                                               kl_use, vl_use, kl_nxt, vl_nxt, ad, ta);
-        if (__builtin_amdgcn_ballot_w64(rep) != 0) PF::repair(st);
+        typename PF::Tmp tp;
+        const bool moved = PF::template iterate<true, VAR, true>(st, sc[par], sc[par ^ 1], pr[par], pr[par ^ 1], fr,
+                                                                 kl_use, vl_use, kl_nxt, vl_nxt, ad, ta, tp);
+        if (__builtin_amdgcn_ballot_w64(moved) != 0) PF::resolve(st, sc[par], pr[par], tp, ta);
       } else {
         PF::prime(fr, kl_nxt, vl_nxt, ad);
       }
@@ -823,14 +869,17 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       phase(n_w + 1, nt + 1, idle);
     }
 
-    // The next item's copies and Q loads go out before this item's output is
+    // The next item's K/V copies go out before this item's output is
     // written, so that their latencies overlap.
     Item nxt;
     const bool more = item_at(round + 1, nxt);
     if (more) start_item(nxt);
 
     // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
-    // head dims 32 db + 8 g + 4 hh + 0..3 of its row.  The scores of the last
+    // head dims 32 db + 8 g + 4 hh + 0..3 of its row; they go to the wave's
+    // staging region in the K-tile layout, come back as whole 16-byte chunks
+    // (1 KB of consecutive rows per instruction) and are stored from there,
+    // rows past Lq falling outside the store's range.  The scores of the last
     // iteration are dead, but are kept live past the padding so that their
     // registers are not reused while the MFMAs writing them are in flight.
     hazard_pad();
@@ -852,12 +901,26 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       uint2 w;
       w.x = PF::E::pack2(agpr_read<a0>() * inv, agpr_read<a0 + 1>() * inv);
       w.y = PF::E::pack2(agpr_read<a0 + 2>() * inv, agpr_read<a0 + 3>() * inv);
-      const int row = row0 + 32 * rb;
-      if (row < Lq) {
-        T* op = reinterpret_cast<T*>(p.o) + ((size_t)cur.head * Lq + row) * D;
-        *reinterpret_cast<uint2*>(op + 32 * db + 8 * g + 4 * hh) = w;
-      }
+      const int r = 32 * rb + n;
+      *reinterpret_cast<uint2*>(qo + r * D + 8 * ((4 * db + g) ^ swz<D>(r)) + 4 * hh) = w;
     });
+    {
+      constexpr int NB = RB * TE * (int)sizeof(T) / 1024;
+      const int left = max(min(Lq - iw, RB * 32), 0) * D * (int)sizeof(T);
+      const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
+          reinterpret_cast<T*>(p.o) + ((size_t)cur.head * Lq + iw) * D, 0, left, 0x00020000);
+      const char* qob = reinterpret_cast<const char*>(qo);
+#pragma unroll
+      for (int blk = 0; blk < NB; ++blk) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(qob + blk * 1024 + lane * 16);
+        const int r = blk * (1024 / (2 * D)) + lane / CPR;
+        const int pos = lane % CPR;
+        __builtin_amdgcn_raw_buffer_store_b128(w, orsrc, (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T), 0, 0);
+      }
+    }
+    // The region is free once its reads have returned: the next item's Q.
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (more) copy_q(nxt);
     if (!more) break;
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     cur = nxt;
