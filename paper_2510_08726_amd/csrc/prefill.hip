@@ -3,54 +3,50 @@
 // the plain attention definition, with the tile structure of the appendix
 // "Privatization" (a local max per key tile, then the running max).
 //
-// Work split.  One workgroup = 4 wave64s = 256 query rows of one (batch,
-// query head); each wave owns 64 rows (two 32-row blocks) for the whole key
-// loop and runs alone on its SIMD with the full register file.  Key tiles
-// are BN = 32 keys.  Per tile j and wave:
+// Work split.  One workgroup = 8 wave64s = 256 query rows of one (batch,
+// query head), two waves per SIMD.  The two waves of a SIMD share 64 rows
+// (two 32-row blocks) for the whole key loop and split the work on them.
+// Key tiles are BN = 32 keys.  Per tile j:
 //
-//   S^T = K_j . Q^T            32x32x16 MFMAs, K from LDS, Q resident in AGPRs
-//   m'  = max(m, rowmax S)     in-lane max + permlane32 swaps
-//   a   = exp2(m - m')         the repair factor h(t, r, r') = t exp(r - r')
-//   P   = exp2(S - m')         rounded to the input type (the compute
-//                              definition casts exp to the input dtype
-//                              before the second matmul)
-//   l   = a l + rowsum P       fp32 sum of the weights before rounding
-//   O^T = a O^T + V_j^T . P^T  32x32x16 MFMAs, V from LDS, P taken straight
-//                              from the S^T accumulator registers
+//   softmax wave  S^T = K_j . Q^T       32x32x16 MFMAs, K from LDS, Q in AGPRs
+//                 P = exp2(S - m)       against the row's reference max m,
+//                                       rounded to the input type (the compute
+//                                       definition casts exp to the input dtype
+//                                       before the second matmul)
+//                 a = exp2(m - m')      only when the tile's max exceeds m by
+//                                       more than the lazy threshold (then m'
+//                                       replaces m and P is recomputed)
+//   P.V wave      O^T = a O^T + V_j^T . P^T,  l = a l + rowsum P
+//                                       32x32x16 MFMAs, V from LDS, O^T and l
+//                                       in AGPRs
 //
-// Computing S transposed puts one query row per lane (rows are the MFMA N
-// index): row reductions stay in registers, the per-row repair of O^T is a
-// per-lane scale, and the fp32 S^T accumulator converts in place into the B
-// operand of the P.V product.  V stays row-major in LDS; its operand is
-// gathered with the gfx950 transposing LDS read, in the key order in which
-// the S^T accumulator holds keys.  Each K or V operand fragment read from
-// LDS feeds the MFMAs of both 32-row blocks, which halves the LDS traffic
-// per flop compared with 32 rows per wave.
+// P and the factors a pass from the softmax wave to its P.V wave through a
+// lane-private LDS exchange buffer.  Computing S transposed puts one query
+// row per lane (rows are the MFMA N index): row reductions stay in
+// registers, the per-row rescale of O^T is a per-lane scale, and the fp32
+// S^T accumulator converts in place into the layout of the B operand of the
+// P.V product.  V stays row-major in LDS; its operand is gathered with the
+// gfx950 transposing LDS read, in the key order in which the S^T accumulator
+// holds keys.  Each K or V operand fragment read from LDS feeds the MFMAs of
+// both 32-row blocks.
 //
-// Schedule.  On gfx950 a wave's VALU instructions issued behind its own
-// MFMA overlap with it, while VALU work of another wave on the same SIMD
-// barely does.  So every wave software-pipelines its own loop: iteration j
-// issues the MFMAs of S^T for tile j+1 and of P.V for tile j-1, and spreads
-// the softmax of tile j (pure VALU, independent of both) over the gaps
-// between them: the iteration is a fixed sequence of MFMA slots, each
-// followed by its share of the softmax and by the LDS reads of the operands
-// a few fragments ahead, fenced so the compiler keeps that order.  K and V
-// tiles are copied HBM -> LDS by the buffer unit (loads with the LDS bit, no
-// registers involved) into double buffers, one tile ahead of their first
-// use; one barrier per iteration publishes them.
+// Schedule.  Iteration j: the softmax wave issues the MFMAs of S^T for tile
+// j+1 back to back, then the softmax of tile j (pure VALU); the P.V wave
+// issues P.V for tile j-1 and the HBM -> LDS copies of K and V (buffer loads
+// with the LDS bit, into rings of kRing tiles).  The P.V MFMAs run on the
+// matrix unit while the softmax wave's VALU work runs beside them; one
+// barrier per iteration publishes the copies and the exchange buffers.
 //
 // The MFMAs are written as inline assembly to fix their register files: the
-// S^T accumulators in VGPRs (the softmax reads them), O^T and Q in AGPRs.
-// The compiler does not model the latency of those instructions, so every
-// VALU reader of an MFMA result is at least two MFMAs and a barrier away
-// from it, or behind explicit s_nop padding.
+// S^T accumulators in VGPRs (the softmax reads them), Q, O^T and l in fixed
+// AGPRs.  The compiler does not model the latency of those instructions;
+// explicit s_nop padding covers it, and a test checks the generated code.
 //
-// Lazy repair.  The running max used in the exponent is only moved when a
-// row's tile max exceeds it by more than 2^8 (in log2 units); until then the
-// stale max keeps every P <= 2^8 (well inside the fp16 / bf16 range) and the
-// O^T repair is skipped.  The repaired state is the same as with an always
-// moving max, written relative to another reference point; the final
-// division by l cancels it.
+// Lazy rescale.  The reference max used in the exponent is only moved when a
+// row's tile max exceeds it by more than 8 (log2 units); until then every
+// P <= 2^8 (well inside the fp16 / bf16 range) and the O^T rescale is
+// skipped.  The state is the same as with an always moving max, written
+// relative to another reference point; the final division by l cancels it.
 //
 // Scores are in log2 units: t = s * scale * log2(e) (+ ALiBi bias * log2(e)),
 // so each exponential is one v_exp_f32.
@@ -67,14 +63,20 @@ namespace attn {
 
 namespace {
 
-constexpr int kWaves = 4;
+// Two waves per SIMD: wave p (p < kPairs) computes S^T and the softmax of
+// its 64 rows, wave p + kPairs (same SIMD) the P.V products and row sums of
+// the same rows.
+constexpr int kPairs = 4;
+constexpr int kWaves = 2 * kPairs;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kCopyWaves = kPairs;          // the P.V waves also issue the HBM -> LDS copies
 constexpr int RB = 2;                       // 32-row blocks per wave
 constexpr int BMW = 32 * RB;                // query rows per wave
 static_assert(RB == 2, "the row-max exchange and the finalisation handle two row blocks");
-constexpr int BM = BMW * kWaves;            // query rows per workgroup
+constexpr int BM = BMW * kPairs;            // query rows per workgroup
 constexpr int BN = 32;                      // keys per tile
-constexpr int PFD = 3;                      // operand fragments read ahead
+constexpr int PFD_K = 1;                    // K fragments read ahead (softmax wave)
+constexpr int PFD_V = 3;                    // V fragments read ahead (P.V wave)
 constexpr int kRing = 4;                    // LDS slots per operand; copies run kRing - 1 tiles ahead
 // A row's reference maximum moves only when a tile's maximum exceeds it by
 // more than this (log2 units), so that P <= 2^kLazyThreshold.
@@ -150,20 +152,23 @@ __device__ __forceinline__ void hazard_pad() {
 }
 
 // Register files.  The S^T accumulators, P and the LDS operands are ordinary
-// values in VGPRs, allocated by the compiler.  O^T, Q, the exp-sums and a
-// constant (1, 1) operand live in fixed AGPRs that only the inline assembly
-// below names: O^T block (rb, db) in a[16 (rb DB + db) .. + 15], Q fragment
-// (rb, kx) in a[128 + 4 (rb KX + kx) .. + 3], l of row block rb in
-// a[192 + 4 rb .. + 3], the ones in a[200 .. 201].
+// values in VGPRs, allocated by the compiler.  The operands that live through
+// the whole key loop are in fixed AGPRs that only the inline assembly below
+// names, per role: in the softmax wave Q fragment (rb, kx) in
+// a[4 (rb KX + kx) .. + 3]; in the P.V wave O^T block (rb, db) in
+// a[16 (rb DB + db) .. + 15], l of row block rb in a[128 + 4 rb .. + 3], the
+// ones in a[136 .. 137].  So at most 138 AGPRs, which leaves 118 VGPRs of a
+// wave's 256 at two waves per SIMD.
 // Every statement that touches them lists all AGPRs as clobbered, so the
 // compiler keeps none of its own values there, and counts them as used.
 #define ATTN_A10(p) "a" #p "0", "a" #p "1", "a" #p "2", "a" #p "3", "a" #p "4", \
                     "a" #p "5", "a" #p "6", "a" #p "7", "a" #p "8", "a" #p "9"
 #define ATTN_AGPRS "a0", "a1", "a2", "a3", "a4", "a5", "a6", "a7", "a8", "a9", \
-    ATTN_A10(1), ATTN_A10(2), ATTN_A10(3), ATTN_A10(4), ATTN_A10(5), ATTN_A10(6), ATTN_A10(7), ATTN_A10(8), ATTN_A10(9), ATTN_A10(10), ATTN_A10(11), ATTN_A10(12), ATTN_A10(13), ATTN_A10(14), ATTN_A10(15), ATTN_A10(16), ATTN_A10(17), ATTN_A10(18), ATTN_A10(19), ATTN_A10(20)
-constexpr int kQAgpr = 128;
-constexpr int kLAgpr = 192;     // exp-sum accumulators, 4 per row block
-constexpr int kOnesAgpr = 200;  // two registers holding (1.0, 1.0)
+    ATTN_A10(1), ATTN_A10(2), ATTN_A10(3), ATTN_A10(4), ATTN_A10(5), ATTN_A10(6), ATTN_A10(7), ATTN_A10(8), ATTN_A10(9), ATTN_A10(10), ATTN_A10(11), ATTN_A10(12), \
+    "a130", "a131", "a132", "a133", "a134", "a135", "a136", "a137"
+constexpr int kQAgpr = 0;
+constexpr int kLAgpr = 128;     // exp-sum accumulators, 4 per row block
+constexpr int kOnesAgpr = 136;  // two registers holding (1.0, 1.0)
 
 // 32x32x16 MFMAs.  qk0/qk: S^T accumulator in VGPRs (qk0 starts from zero), K
 // operand in VGPRs, Q operand from AGPRs a[QA .. QA + 3].  pv: O^T accumulator
@@ -235,12 +240,11 @@ __device__ __forceinline__ void static_for(F&& f) {
       std::make_integer_sequence<int, N>{});
 }
 
-// The softmax of one tile as a list of steps, spread over the MFMA slots of
-// an iteration in proportion to their VALU cost (in issue cycles):
+// The softmax of one tile as a list of steps (weights are their VALU cost in
+// issue cycles, used to spread steps over MFMA slots where that is wanted):
 //   prep   4 steps (ALiBi or masked tiles): bias and mask of 4 keys x 2 rows
-//   max    8 steps: 4 scores folded into the partial max of a row block
-//   fin    1 step : row maxima, lazy decisions, repair factors
 //   exp   16 steps: 2 exponentials and their packing
+//   max    8 steps: 4 scores folded into this lane's partial max of a row block
 // (the exp-sum is accumulated by rowsum MFMAs beside P.V).
 template <bool PREP, bool MASKED, bool ALIBI>
 struct SoftPlan {
@@ -277,11 +281,11 @@ struct Prefill {
   static constexpr int KX = D / 16;                        // MFMA K-steps of Q.K^T
   static constexpr int DB = D / 32;                        // 32-dim blocks of O^T
   static constexpr int TE = BN * D;                        // elements of one K or V tile
-  static constexpr int NI = TE * (int)sizeof(T) / 1024 / kWaves;  // 1 KB copies per wave per tile
+  static constexpr int NI = TE * (int)sizeof(T) / 1024 / kCopyWaves;  // 1 KB copies per copying wave per tile
   static constexpr int CPR = D / 8;                        // 16-byte chunks per row
   static constexpr int NG = KX;                            // K (or V) operand fragments per tile
   static_assert(NG == 2 * DB, "as many V fragments as K fragments");
-  static_assert(NI >= 1, "a tile is at least one 1 KB copy per wave");
+  static_assert(NI >= 1, "a tile is at least one 1 KB copy per copying wave");
 
   // S^T accumulators of one tile: s[rb] holds keys 0..31 of row block rb.
   // Register r of lane (n, hh) is key 8 (r / 4) + 4 hh + r % 4 of row 32 rb + n.
@@ -298,6 +302,7 @@ struct Prefill {
   };
   static constexpr int oagpr(int rb, int db) { return 16 * (rb * DB + db); }
   static constexpr int qagpr(int rb, int kx) { return kQAgpr + 4 * (rb * KX + kx); }
+  static_assert(16 * RB * DB <= kLAgpr && kQAgpr + 4 * RB * KX <= kLAgpr, "AGPR map");
   // Per-lane LDS byte offsets inside a tile: K fragment kx, V fragment
   // (c16, db); c16 only adds an immediate.
   struct Addr {
@@ -313,16 +318,18 @@ struct Prefill {
     float sl2;    // ALiBi slope * log2(e)
     float abase;  // ALiBi bias of key j0 + 4 hh relative to the wave's first row
     int lim[RB];  // last visible key offset (key - j0 - 4 hh) of each row block
+    u32x4* xp;    // this lane's exchange units for the tile's P (unit rb * 2 + c16, stride 64)
   };
 
   // HBM -> LDS copy of key/value tile t (rows t BN .. t BN + BN - 1) of one
-  // head into the LDS slot at byte address `slot`: copy u of wave w fills the
-  // 1 KB block u kWaves + w; dof holds the lane's global byte offsets.  The
+  // head into the LDS slot at byte address `slot`: copy u of copying wave cw
+  // fills the 1 KB block u kCopyWaves + cw; dof holds the lane's global byte
+  // offsets.  The
   // buffer range ends at row `rows` (the workgroup's last staged row), so rows
   // past it read as zero, and a tile past it moves no data at all.  Issued as
   // inline assembly: the compiler then adds no waits of its own for the LDS
   // writes; the kernel waits for them explicitly before its barriers.
-  static __device__ __forceinline__ void copy_tile(const T* base, uint32_t slot, int t, int rows, int wave,
+  static __device__ __forceinline__ void copy_tile(const T* base, uint32_t slot, int t, int rows, int cw,
                                                    const int (&dof)[NI]) {
     const int left = t >= 0 ? max(rows - t * BN, 0) : 0;
     const uint64_t a = reinterpret_cast<uint64_t>(base + (left > 0 ? (size_t)t * TE : 0));
@@ -334,33 +341,15 @@ struct Prefill {
 #pragma unroll
     for (int u = 0; u < NI; ++u)
       asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                   : : "s"(slot + (uint32_t)((u * kWaves + wave) * 1024)), "v"(dof[u]), "s"(rsrc) : "memory", "m0");
+                   : : "s"(slot + (uint32_t)((u * kCopyWaves + cw) * 1024)), "v"(dof[u]), "s"(rsrc) : "memory", "m0");
   }
 
-  // This wave's copy of the RB * 32 rows at `base` into its LDS region at
-  // byte address `dst`, in the layout of a K tile (row r at r * D elements,
-  // chunk c at chunk position c ^ swz(r)); rows at or past `left` read as
-  // zero.  Only the copying wave reads the region.
-  static __device__ __forceinline__ void copy_rows(const T* base, uint32_t dst, int left, int lane) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    const int nb = max(min(left, RB * 32), 0) * D * (int)sizeof(T);
-    const u32x4 rsrc = {(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
-                        (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
-                        (uint32_t)__builtin_amdgcn_readfirstlane(nb), 0x00020000u};
-#pragma unroll
-    for (int blk = 0; blk < RB * TE * (int)sizeof(T) / 1024; ++blk) {
-      const int r = blk * (1024 / (2 * D)) + lane / CPR;
-      const int pos = lane % CPR;
-      const int goff = (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T);
-      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                   : : "s"(dst + (uint32_t)(blk * 1024)), "v"(goff), "s"(rsrc) : "memory", "m0");
-    }
-  }
-
-  static __device__ __forceinline__ void make_addr(Addr& ad, int lane) {
+  static __device__ __forceinline__ void make_addr_k(Addr& ad, int lane) {
     const int n = lane & 31, hh = lane >> 5;
 #pragma unroll
     for (int kx = 0; kx < KX; ++kx) ad.k[kx] = 2 * (n * D + 8 * ((2 * kx + hh) ^ swz<D>(n)));
+  }
+  static __device__ __forceinline__ void make_addr_v(Addr& ad, int lane) {
     const int G = lane >> 4, i = lane & 15;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -433,6 +422,11 @@ struct Prefill {
       uint32_t w = E::pack2(p0, p1);
       pin(w);
       pr.w[rb][r / 8][(r % 8) / 2] = w;
+      // A complete 16-key slice of P goes to the exchange buffer at once.
+      if constexpr (r % 8 == 6) {
+        const u32x4 u = {pr.w[rb][r / 8][0], pr.w[rb][r / 8][1], pr.w[rb][r / 8][2], pr.w[rb][r / 8][3]};
+        ta.xp[64 * (rb * 2 + r / 8)] = u;
+      }
     } else {
       constexpr int k = P::max_index(K);
       constexpr int q = k / 2, rb = k % 2;
@@ -458,10 +452,11 @@ struct Prefill {
   // Slow path of a tile whose maximum moved past the threshold in some row
   // of the wave (always the case for a row's first visible tile, whose
   // reference is still kMcInit): the row maximum is combined over the lane
-  // pair holding the row, rows that moved take it as their new reference,
-  // O^T and l are rescaled by 2^-(move) (the P.V products so far used the
-  // old reference), and the tile's P is recomputed.  Rows that did not move
-  // keep their reference and factor 1.
+  // pair holding the row, rows that moved take it as their new reference
+  // and the factor 2^-(move) by which the P.V wave rescales O^T and l before
+  // it adds this tile (the products so far used the old reference), and the
+  // tile's P is recomputed.  Rows that did not move keep their reference and
+  // factor 1.
   static __device__ __forceinline__ void resolve(State& st, Scores& sc, Probs& pr, Tmp& tp, const TileArgs& ta) {
     typedef SoftPlan<false, false, ALIBI> P;
     const float ce = ALIBI ? 1.f : ta.c;
@@ -475,7 +470,6 @@ struct Prefill {
       st.alpha[rb] = move ? fast_exp2(-d) : 1.f;
       st.mc[rb] = move ? tm[rb] * ce : st.mc[rb];
     }
-    repair(st);
     static_for<P::NSTEP>([&](auto kc) {
       constexpr int K = decltype(kc)::value;
       if constexpr (P::is_exp(K)) soft_step<K, false, false>(st, sc, pr, tp, ta);
@@ -491,99 +485,116 @@ struct Prefill {
     }
   }
 
-  // Fragment i of an iteration: group i / 2, the K fragment of the group
-  // first, then its V fragment.  Fragment i lives in ring entry i mod
-  // (PFD + 1) and is read PFD fragments ahead of its MFMAs; the first PFD
-  // fragments of an iteration are read at the end of the iteration before.
-  static constexpr int NF = 2 * NG;   // fragments per iteration
-  static_assert(NF % (PFD + 1) == 0, "fragment ring positions must repeat every iteration");
-  // LDS instructions that read the first PFD fragments (a K fragment takes
-  // one, a V fragment two).
-  static constexpr int kPrimeReads = (PFD + 1) / 2 + 2 * (PFD / 2);
-  typedef vec8 Ring[PFD + 1];
+  // Operand fragments: an iteration of either wave uses NG fragments, K
+  // fragments (kx = 0..NG-1) for S^T, V fragments (g = c16 DB + db) for P.V.
+  // Fragment i lives in ring entry i mod (PFD + 1) and is read PFD fragments
+  // ahead of its MFMAs; the first PFD fragments of an iteration are read at
+  // the end of the iteration before.
+  template <bool IS_K> static constexpr int pfd() { return IS_K ? PFD_K : PFD_V; }
+  static_assert(NG % (PFD_K + 1) == 0 && NG % (PFD_V + 1) == 0, "fragment ring positions must repeat every iteration");
+  template <bool IS_K> using Ring = vec8[pfd<IS_K>() + 1];
+  // LDS instructions that read the first fragments of an iteration.
+  static constexpr int kPrimeK = PFD_K;
+  static constexpr int kPrimeV = 2 * PFD_V;
 
-  template <int I>
-  static __device__ __forceinline__ void read_frag(Ring& fr, const T* kl, const T* vl, const Addr& ad) {
-    if constexpr (I % 2 == 0) fr[I % (PFD + 1)] = kfrag(kl, ad, I / 2);
-    else fr[I % (PFD + 1)] = vfrag(vl, ad, I / 2);
+  template <bool IS_K, int I>
+  static __device__ __forceinline__ void read_frag(Ring<IS_K>& fr, const T* tile, const Addr& ad) {
+    if constexpr (IS_K) fr[I % (PFD_K + 1)] = kfrag(tile, ad, I);
+    else fr[I % (PFD_V + 1)] = vfrag(tile, ad, I);
   }
-  // The first PFD fragments of the iteration whose tiles are kl and vl.
-  static __device__ __forceinline__ void prime(Ring& fr, const T* kl, const T* vl, const Addr& ad) {
-    static_for<PFD>([&](auto ic) { read_frag<decltype(ic)::value>(fr, kl, vl, ad); });
+  template <bool IS_K>
+  static __device__ __forceinline__ void prime(Ring<IS_K>& fr, const T* tile, const Addr& ad) {
+    static_for<pfd<IS_K>()>([&](auto ic) { read_frag<IS_K, decltype(ic)::value>(fr, tile, ad); });
   }
 
-  // One iteration of the software pipeline: S^T of tile j+1 (QK), softmax of
-  // tile j (SM: 1 unmasked, 2 masked), P.V of tile j-1 (PV).  Group g holds
-  // the slots [QK rb 0, QK rb 1, PV rb 0, PV rb 1] of K fragment g and V
-  // fragment g.  kl, vl are this iteration's K and V tiles, kln, vln the next
-  // iteration's (its first fragments are read in the last slots).
-
-  template <bool QK, int SM, bool PV>
-  static __device__ __forceinline__ bool iterate(State& st, Scores& s_cur, Scores& s_next, Probs& p_cur,
-                                                 const Probs& p_prev, Ring& fr, const T* kl, const T* vl,
-                                                 const T* kln, const T* vln, const Addr& ad, const TileArgs& ta,
-                                                 Tmp& tp) {
-    static_assert(QK && PV, "every iteration issues both products");
+  // One iteration of the softmax wave: the 2 NG MFMAs of S^T of tile j+1 (kl:
+  // its K tile; order [kx, rb]) back to back, then the softmax of tile j (SM:
+  // 1 unmasked, 2 masked); kln is the next iteration's K tile, whose first
+  // fragments are read during the last MFMAs.  Returns whether some score of
+  // this lane exceeds its row's reference by more than the threshold.  (The
+  // partner P.V wave's MFMAs fill the matrix unit while this wave runs its
+  // VALU work; interleaving both kinds in this wave stalled it whenever the
+  // partner's MFMAs held the matrix unit.)
+  template <int SM>
+  static __device__ __forceinline__ bool iterate_s(State& st, Scores& s_cur, Scores& s_next, Probs& p_cur,
+                                                   Ring<true>& fr, const T* kl, const T* kln,
+                                                   const Addr& ad, const TileArgs& ta, Tmp& tp) {
     constexpr bool MASKED = SM == 2;
     constexpr bool PREP = ALIBI || MASKED;
     typedef SoftPlan<PREP, MASKED, ALIBI> P;
-    constexpr int FPG = 2;        // fragments per group
-    constexpr int NS = 2 * NF;    // MFMA slots
-    // Fragments NF .. NF + PFD - 1 are the first ones of the next iteration.
+    constexpr int NS = 2 * NG;
     auto read = [&](auto ic) {
       constexpr int i = decltype(ic)::value;
-      if constexpr (i < NF) read_frag<i>(fr, kl, vl, ad);
-      else read_frag<i - NF>(fr, kln, vln, ad);
+      if constexpr (i < NG) read_frag<true, i>(fr, kl, ad);
+      else read_frag<true, i - NG>(fr, kln, ad);
     };
-    {
-      [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
-        (
-            [&] {
-              constexpr int S = Ss;
-              constexpr int i = S / 2, rb = S % 2;
-              constexpr int g = i / FPG;
-              constexpr bool is_k = QK && (i % FPG == 0);
-              if constexpr (rb == 0) read(std::integral_constant<int, i + PFD>{});
-              if constexpr (is_k) {
-                if constexpr (g == 0) M::template qk0<qagpr(rb, g)>(s_next.s[rb], fr[i % (PFD + 1)]);
-                else M::template qk<qagpr(rb, g)>(s_next.s[rb], fr[i % (PFD + 1)]);
-              } else {
-                constexpr int c16 = g / DB, db = g % DB;
-                M::template pv<oagpr(rb, db)>(fr[i % (PFD + 1)], probs_b(p_prev, rb, c16));
-                // Exp-sum of the same weights: words 2 db, 2 db + 1 of the
-                // slice, at fragments db = 0 and 1 (a large MFMA always
-                // separates two rowsum MFMAs on one accumulator).
-                if constexpr (db < 2)
-                  M::template rowsum<kLAgpr + 4 * rb>(
-                      make_uint2(p_prev.w[rb][c16][2 * db], p_prev.w[rb][c16][2 * db + 1]));
-              }
-              if constexpr (SM != 0)
-                soft_range<P::begin(S, NS), P::begin(S + 1, NS), PREP, MASKED>(st, s_cur, p_cur, tp, ta);
-              __builtin_amdgcn_sched_barrier(0);
-            }(),
-            ...);
-      }(std::make_integer_sequence<int, NS>{});
-    }
-    return exceeds(st, tp, ta);
+    [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
+      (
+          [&] {
+            constexpr int S = Ss;
+            constexpr int kx = S / 2, rb = S % 2;
+            if constexpr (rb == 0) read(std::integral_constant<int, kx + PFD_K>{});
+            if constexpr (kx == 0) M::template qk0<qagpr(rb, kx)>(s_next.s[rb], fr[kx % (PFD_K + 1)]);
+            else M::template qk<qagpr(rb, kx)>(s_next.s[rb], fr[kx % (PFD_K + 1)]);
+          }(),
+          ...);
+    }(std::make_integer_sequence<int, NS>{});
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (SM != 0) soft_range<0, P::NSTEP, PREP, MASKED>(st, s_cur, p_cur, tp, ta);
+    if constexpr (SM != 0) return exceeds(st, tp, ta);
+    return false;
   }
 
-  // O^T *= alpha and l *= alpha, in place in the AGPRs.
-  static __device__ __forceinline__ void repair(const State& st) {
+  // One iteration of the P.V wave: O^T += V^T P^T of tile j-1 (vl: its V
+  // tile; the 2 NG slots are [g, rb], g = c16 DB + db) with the row sums of
+  // the same weights; vln is the next iteration's V tile.
+  static __device__ __forceinline__ void iterate_o(const Probs& pr, Ring<false>& fr, const T* vl, const T* vln,
+                                                   const Addr& ad) {
+    constexpr int NS = 2 * NG;
+    auto read = [&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (i < NG) read_frag<false, i>(fr, vl, ad);
+      else read_frag<false, i - NG>(fr, vln, ad);
+    };
+    [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
+      (
+          [&] {
+            constexpr int S = Ss;
+            constexpr int g = S / 2, rb = S % 2;
+            constexpr int c16 = g / DB, db = g % DB;
+            if constexpr (rb == 0) read(std::integral_constant<int, g + PFD_V>{});
+            M::template pv<oagpr(rb, db)>(fr[g % (PFD_V + 1)], probs_b(pr, rb, c16));
+            // Exp-sum of the same weights: words 2 db, 2 db + 1 of the slice,
+            // at fragments db = 0 and 1 (a large MFMA always separates two
+            // rowsum MFMAs on one accumulator).
+            if constexpr (db < 2)
+              M::template rowsum<kLAgpr + 4 * rb>(make_uint2(pr.w[rb][c16][2 * db], pr.w[rb][c16][2 * db + 1]));
+            __builtin_amdgcn_sched_barrier(0);
+          }(),
+          ...);
+    }(std::make_integer_sequence<int, NS>{});
+  }
+
+  // O^T *= alpha and l *= alpha, in place in the P.V wave's AGPRs.
+  static __device__ __forceinline__ void repair(const float (&alpha)[RB]) {
     hazard_pad();
     static_for<RB * DB * 16>([&](auto ic) {
       constexpr int e = decltype(ic)::value;
-      agpr_scale<e>(st.alpha[e / (16 * DB)]);
+      agpr_scale<e>(alpha[e / (16 * DB)]);
     });
     static_for<RB * 4>([&](auto ic) {
       constexpr int e = decltype(ic)::value;
-      agpr_scale<kLAgpr + e>(st.alpha[e / 4]);
+      agpr_scale<kLAgpr + e>(alpha[e / 4]);
     });
     hazard_pad();
   }
 };
 
+// Two waves per SIMD leave each wave 256 registers: the 138 AGPRs named by
+// the inline assembly and at most 116 VGPRs (the compiler does not subtract
+// the inline assembly's AGPRs from its budget by itself).
 template <int D, typename T, bool CAUSAL, bool ALIBI>
-__global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
+__global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(116))) void prefill_kernel(PrefillParams p) {
   typedef Prefill<D, T, CAUSAL, ALIBI> PF;
   constexpr bool REV = ALIBI;
   typedef typename PF::vec8 vec8;
@@ -593,33 +604,27 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   typedef typename PF::Addr Addr;
   typedef typename PF::TileArgs TileArgs;
   constexpr int KX = PF::KX;
+  constexpr int DB = PF::DB;
   constexpr int TE = PF::TE;
   constexpr int NI = PF::NI;
   constexpr int CPR = PF::CPR;
-  // LDS: a ring of kRing K tiles, a ring of kRing V tiles, then one region
-  // of RB * 32 rows per wave that stages its Q block in and its O block out.
-  __shared__ __attribute__((aligned(1024))) T lds[2 * kRing * TE + kWaves * RB * TE];
+  // LDS: a ring of kRing K tiles, a ring of kRing V tiles, then per pair of
+  // waves two exchange buffers (tile parity) in which the softmax wave leaves
+  // P (units rb * 2 + c16: the four words of slice c16 of row block rb) and
+  // the rescale factors (unit 2 RB) for its P.V wave, 16 bytes per lane and
+  // unit, lane-private.
+  constexpr int XU = 2 * RB + 1;
+  __shared__ __attribute__((aligned(1024))) T lds[2 * kRing * TE];
+  __shared__ __attribute__((aligned(16))) u32x4 xch[kPairs][2][XU][64];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int pair = wave & (kPairs - 1);
+  const bool soft_wave = wave < kPairs;
   const int n = lane & 31;
   const int hh = lane >> 5;
 
-  Addr ad;
-  PF::make_addr(ad, lane);
-  // Global offsets of this lane's HBM -> LDS copies: in copy u the lane writes
-  // bytes 16 lane .. 16 lane + 15 of 1 KB block u * kWaves + wave, i.e. chunk
-  // position lane % CPR of row (block * 1024 / (2 D) + lane / CPR), and reads
-  // the global chunk that the swizzle puts there.
-  int dof[NI];
-#pragma unroll
-  for (int u = 0; u < NI; ++u) {
-    const int blk = u * kWaves + wave;
-    const int r = blk * (1024 / (2 * D)) + lane / CPR;
-    const int pos = lane % CPR;
-    dof[u] = (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T);
-  }
   // LDS byte addresses of the K and V slots.
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)lds;
   auto kslot = [&](int s) __attribute__((always_inline)) { return lds0 + (uint32_t)(s * TE * (int)sizeof(T)); };
@@ -649,8 +654,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   const int off = Lk - Lq;
 
   // One work item: its query block and head, and the key tiles [0, nt) that
-  // the workgroup stages, [0, n_w) that this wave computes and [0, fm_w) that
-  // no row of this wave masks.
+  // the workgroup stages, [0, n_w) that this pair of waves computes and
+  // [0, fm_w) that no row of the pair masks.
   struct Item {
     int qb, head, kvh, hq, iw, nt, n_w, fm_w, rows;
   };
@@ -664,7 +669,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     it.head = it.kvh * p.group + rem % p.group;
     it.hq = it.head % p.Hq;
     const int i0 = it.qb * BM;
-    it.iw = i0 + BMW * wave;
+    it.iw = i0 + BMW * pair;
     int kend = Lk, kend_w = Lk;
     if (CAUSAL) {
       kend = min(Lk, min(i0 + BM, Lq) + off);
@@ -679,12 +684,6 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     it.rows = min(Lk, it.nt * BN);
     return true;
   };
-  auto kbase = [&](const Item& it) __attribute__((always_inline)) {
-    return reinterpret_cast<const T*>(p.k) + (size_t)it.kvh * Lk * D;
-  };
-  auto vbase = [&](const Item& it) __attribute__((always_inline)) {
-    return reinterpret_cast<const T*>(p.v) + (size_t)it.kvh * Lk * D;
-  };
   // Iteration j handles key tile tile(j).  With ALiBi the tiles are visited
   // from the last to the first: the bias grows with the key index, so the
   // first tile holds the largest bias of each row and the running maximum
@@ -692,154 +691,25 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   // rescale of O^T).  Otherwise the keys run forward.
   auto tile_of = [&](const Item& it, int j) __attribute__((always_inline)) { return REV ? it.nt - 1 - j : j; };
 
-  // Start of an item: the V slots of iterations -1 and -2 zeroed (the first
-  // two iterations multiply them by P = 0) and the copies of the K tiles of
-  // iterations 0 .. kRing-2 and of the V tile of iteration 0 issued.  It runs
-  // after the barrier that ends the previous item's last LDS reads, while the
-  // previous item's output is still being written; the caller waits for it.
-  auto start_item = [&](const Item& it) __attribute__((always_inline)) {
-    {
-      constexpr int NV16 = TE * (int)sizeof(T) / 16;
-      uint4* vz = reinterpret_cast<uint4*>(lds + (kRing + kRing - 2) * TE);   // slots kRing-2, kRing-1
-#pragma unroll
-      for (int i = tid; i < 2 * NV16; i += kThreads) vz[i] = make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int j = 0; j < kRing - 1; ++j) PF::copy_tile(kbase(it), kslot(j), tile_of(it, j), it.rows, wave, dof);
-    PF::copy_tile(vbase(it), vslot(0), tile_of(it, 0), it.rows, wave, dof);
-  };
-  // This wave's staging region (Q rows in, O rows out) and the copy of an
-  // item's Q rows into it; the region's previous contents must have been read.
-  T* const qo = lds + 2 * kRing * TE + wave * RB * TE;
-  const uint32_t qo_addr = (uint32_t)(uintptr_t)(lds_void*)qo;
-  auto copy_q = [&](const Item& it) __attribute__((always_inline)) {
-    PF::copy_rows(reinterpret_cast<const T*>(p.q) + ((size_t)it.head * Lq + it.iw) * D, qo_addr, Lq - it.iw, lane);
-  };
+  const std::integral_constant<int, 0> idle;
+  const std::integral_constant<int, 1> whole;
+  const std::integral_constant<int, 2> masked;
 
   Item cur;
   if (!item_at(0, cur)) return;
-  start_item(cur);
-  copy_q(cur);
-  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  agpr_write<kOnesAgpr>(PF::M::kOnes);
-  agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
 
   for (int round = 0;; ++round) {
     const int nt = cur.nt, n_w = cur.n_w, fm_w = cur.fm_w;
     const int iw = cur.iw;
     const int row0 = iw + n;          // this lane's row in row block 0
-    const T* kp = kbase(cur);
-    const T* vp = vbase(cur);
-
-    // Q fragments (B operand of S^T: lane (n, hh) holds Q[row][16 kx + 8 hh
-    // + 0..7], read like K fragments) into their AGPRs, negated for a
-    // negative scale; O^T and l start at zero.
-    static_for<RB * KX>([&](auto ic) {
-      constexpr int f = decltype(ic)::value;
-      constexpr int rb = f / KX, kx = f % KX;
-      const u32x4 w = __builtin_bit_cast(u32x4, PF::kfrag(qo + rb * TE, ad, kx));
-      agpr_write<PF::qagpr(rb, kx) + 0>(w[0] ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 1>(w[1] ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 2>(w[2] ^ p.qsign);
-      agpr_write<PF::qagpr(rb, kx) + 3>(w[3] ^ p.qsign);
-    });
-    static_for<RB * PF::DB * 16>([&](auto ic) { agpr_zero<decltype(ic)::value>(); });
-    static_for<RB * 4>([&](auto ic) { agpr_zero<kLAgpr + decltype(ic)::value>(); });
-    State st;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      st.mc[rb] = kMcInit;
-      st.alpha[rb] = 1.f;
-    }
+    const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)cur.kvh * Lk * D;
+    const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)cur.kvh * Lk * D;
     auto tile = [&](int j) __attribute__((always_inline)) { return tile_of(cur, j); };
-    auto copy_tile = [&](const T* base, uint32_t slot, int j) __attribute__((always_inline)) {
-      PF::copy_tile(base, slot, tile(j), cur.rows, wave, dof);
-    };
-
-    TileArgs ta;
-    ta.c = p.c;
-    ta.sl2 = ALIBI ? p.slopes[cur.hq] * kLog2e : 0.f;
-    // Per-tile softmax parameters.  Tiles outside [0, n_w) are fully masked
-    // (lim = -1): their softmax leaves the state unchanged and gives P = 0.
-    auto set_tile = [&](int j) __attribute__((always_inline)) {
-      const int t = tile(j);
-      const int j0 = t * BN;
-      ta.abase = ALIBI ? ta.sl2 * (float)(j0 + 4 * hh - iw - off) : 0.f;
-      const bool live = t >= 0 && t < n_w;
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        int l = Lk - 1 - j0 - 4 * hh;
-        if (CAUSAL) l = min(l, row0 + 32 * rb + off - j0 - 4 * hh);
-        ta.lim[rb] = live ? l : -1;
-      }
-    };
-
-    Scores sc[2];
-    Probs pr[2];
-    typename PF::Ring fr;
-    // P of iteration -2 is zero (iteration -1 writes a zero P as well, and
-    // idle iterations leave both in place).  Pinned, so that the zeros are
-    // materialised in VGPRs here and not just before the first P.V MFMA that
-    // reads them.
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          uint32_t z = 0u;
-          pin(z);
-          pr[0].w[rb][cc][w] = z;
-        }
-
-    // Iteration j (from -1; "tile j" below is tile(j)): copies of K_{j+kRing}
-    // and V_{j+kRing-2}; S^T of tile j+1, softmax of tile j, P.V of tile j-1,
-    // then, if tile j's maximum moved past the threshold in some row of the
-    // wave, the slow path (rescale of O^T and l, P recomputed).  The K or V tile of iteration j lives in
-    // slot j mod kRing.  A tile's first fragments are read at the end of the
-    // iteration before its use, so its copy, issued kRing - 1 iterations
-    // before its use into the slot read by the iteration before, must be
-    // complete at the barrier that ends the iteration two before its use:
-    // vmcnt lets only the current iteration's copies stay in flight (every
-    // iteration issues the same number of copies), and lgkmcnt lets the reads
-    // of the next iteration's first fragments, which touch neither slot
-    // copied into next, cross the barrier.  The scores and probabilities of
-    // iteration j live in the register buffers of the parity of j.  VAR is 1
-    // for tiles every row of the wave sees whole, 2 for masked tiles
-    // (including the tiles outside [0, n_w), whose softmax is a no-op: P = 0,
-    // K unused), 0 for iterations in which the wave has no S^T, softmax or
-    // P.V to do (copies, the next iteration's first fragments and the
-    // barrier only).
-    auto iteration = [&](int j, auto var, auto slotc) __attribute__((always_inline)) {
-      constexpr int VAR = decltype(var)::value;
-      constexpr int k = decltype(slotc)::value;   // j mod kRing
-      constexpr int par = k & 1;
-      copy_tile(kp, kslot(k), j + kRing);
-      copy_tile(vp, vslot((k + kRing - 2) % kRing), j + kRing - 2);
-      const T* kl_nxt = lds + ((k + 2) % kRing) * TE;   // K_{j+2}
-      const T* vl_nxt = lds + (kRing + k) * TE;         // V_j
-      if constexpr (VAR != 0) {
-        set_tile(j);
-        const T* kl_use = lds + ((k + 1) % kRing) * TE;                  // K_{j+1}
-        const T* vl_use = lds + (kRing + (k + kRing - 1) % kRing) * TE;  // V_{j-1}
-        typename PF::Tmp tp;
-        const bool moved = PF::template iterate<true, VAR, true>(st, sc[par], sc[par ^ 1], pr[par], pr[par ^ 1], fr,
-                                                                 kl_use, vl_use, kl_nxt, vl_nxt, ad, ta, tp);
-        if (__builtin_amdgcn_ballot_w64(moved) != 0) PF::resolve(st, sc[par], pr[par], tp, ta);
-      } else {
-        PF::prime(fr, kl_nxt, vl_nxt, ad);
-      }
-      // 16 wait states between this iteration's last MFMAs and the next
-      // iteration's first reads of their results, the waits described above,
-      // then the barrier that publishes the completed copies.
-      asm volatile("s_nop 7\n\ts_nop 7\n\ts_waitcnt vmcnt(%0) lgkmcnt(%1)\n\ts_barrier"
-                   : : "n"(2 * NI), "n"(PF::kPrimeReads) : "memory");
-    };
     // Iterations j in [j0, j1), j0 >= 0, of one variant; the loop body is
     // unrolled by kRing so that slots and parities are compile-time choices.
     // Every iteration of every wave ends in one barrier, so the waves of the
     // workgroup stay in step whatever their phase boundaries.
-    auto phase = [&](int j0, int j1, auto var) __attribute__((always_inline)) {
+    auto phase = [&](auto& iteration, int j0, int j1, auto var) __attribute__((always_inline)) {
       for (int jb = j0 & ~(kRing - 1); jb < j1; jb += kRing) {
         static_for<kRing>([&](auto kc) __attribute__((always_inline)) {
           const int j = jb + decltype(kc)::value;
@@ -848,81 +718,229 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
       }
     };
 
-    const std::integral_constant<int, 0> idle;
-    const std::integral_constant<int, 1> whole;
-    const std::integral_constant<int, 2> masked;
-    // The first fragments of iteration -1: K_0 and the zeroed V slot.
-    PF::prime(fr, lds, lds + (kRing + kRing - 2) * TE, ad);
-    iteration(-1, masked, std::integral_constant<int, kRing - 1>{});
-    if constexpr (REV) {
-      // Tiles [n_w + 1, nt) first (nothing to do), then n_w (its S^T of
-      // tile n_w - 1 is the first needed), the masked tiles [fm_w, n_w), the
-      // whole tiles, and the P.V of tile 0.
-      const int a = max(0, nt - n_w - 1);
-      phase(0, a, idle);
-      phase(a, nt - fm_w, masked);
-      phase(nt - fm_w, nt, whole);
-      phase(nt, nt + 1, masked);
+    if (soft_wave) {
+      // ---- softmax wave: S^T of tile j+1 and the softmax of tile j ----
+      Addr ad;
+      PF::make_addr_k(ad, lane);
+      // Q fragments (B operand of S^T: lane (n, hh) holds Q[row][16 kx + 8 hh
+      // + 0..7]) into their AGPRs, negated for a negative scale.
+      {
+        const T* qp = reinterpret_cast<const T*>(p.q) + (size_t)cur.head * Lq * D;
+        static_for<RB * KX>([&](auto ic) {
+          constexpr int f = decltype(ic)::value;
+          constexpr int rb = f / KX, kx = f % KX;
+          const int row = row0 + 32 * rb;
+          u32x4 w = {0u, 0u, 0u, 0u};
+          if (row < Lq) w = *reinterpret_cast<const u32x4*>(qp + (size_t)row * D + 16 * kx + 8 * hh);
+          agpr_write<PF::qagpr(rb, kx) + 0>(w[0] ^ p.qsign);
+          agpr_write<PF::qagpr(rb, kx) + 1>(w[1] ^ p.qsign);
+          agpr_write<PF::qagpr(rb, kx) + 2>(w[2] ^ p.qsign);
+          agpr_write<PF::qagpr(rb, kx) + 3>(w[3] ^ p.qsign);
+        });
+      }
+      State st;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        st.mc[rb] = kMcInit;
+        st.alpha[rb] = 1.f;
+      }
+      TileArgs ta;
+      ta.c = p.c;
+      ta.sl2 = ALIBI ? p.slopes[cur.hq] * kLog2e : 0.f;
+      // Per-tile softmax parameters.  Tiles outside [0, n_w) are fully masked
+      // (lim = -1): their softmax leaves the state unchanged and gives P = 0.
+      auto set_tile = [&](int j) __attribute__((always_inline)) {
+        const int t = tile(j);
+        const int j0 = t * BN;
+        ta.abase = ALIBI ? ta.sl2 * (float)(j0 + 4 * hh - iw - off) : 0.f;
+        const bool live = t >= 0 && t < n_w;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          int l = Lk - 1 - j0 - 4 * hh;
+          if (CAUSAL) l = min(l, row0 + 32 * rb + off - j0 - 4 * hh);
+          ta.lim[rb] = live ? l : -1;
+        }
+      };
+      Scores sc[2];
+      Probs pr;
+      typename PF::template Ring<true> fr;
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      // The first fragments of iteration -1: K_0.
+      PF::template prime<true>(fr, lds, ad);
+      // Iteration j (from -1; "tile j" below is tile(j)): S^T of tile j+1 from
+      // the K slot (j+1) mod kRing, softmax of tile j (VAR 1 whole, 2 masked,
+      // 0 none), then, if the tile's maximum moved past the threshold in some
+      // row of the wave, the slow path; P and the rescale factors go to the
+      // exchange buffer of parity j.  The barrier that ends the iteration
+      // publishes them to the P.V wave, whose iteration j+1 uses them.
+      auto iteration = [&](int j, auto var, auto slotc) __attribute__((always_inline)) {
+        constexpr int VAR = decltype(var)::value;
+        constexpr int k = decltype(slotc)::value;   // j mod kRing
+        constexpr int par = k & 1;
+        const T* kl_use = lds + ((k + 1) % kRing) * TE;   // K_{j+1}
+        const T* kl_nxt = lds + ((k + 2) % kRing) * TE;   // K_{j+2}
+        if constexpr (VAR != 0) {
+          set_tile(j);
+          ta.xp = &xch[pair][par][0][lane];
+          typename PF::Tmp tp;
+          const bool moved = PF::template iterate_s<VAR>(st, sc[par], sc[par ^ 1], pr, fr, kl_use, kl_nxt,
+                                                          ad, ta, tp);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) st.alpha[rb] = 1.f;
+          if (__builtin_amdgcn_ballot_w64(moved) != 0) PF::resolve(st, sc[par], pr, tp, ta);
+          const u32x4 a = {as_u(st.alpha[0]), as_u(st.alpha[1]), 0u, 0u};
+          xch[pair][par][2 * RB][lane] = a;
+        } else {
+          PF::template prime<true>(fr, kl_nxt, ad);
+        }
+        // 16 wait states between this iteration's last MFMAs and the next
+        // iteration's first reads of their results; this wave's LDS traffic
+        // complete; then the barrier.
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      };
+      iteration(-1, masked, std::integral_constant<int, kRing - 1>{});
+      if constexpr (REV) {
+        // Tiles [n_w + 1, nt) first (nothing to do), then n_w (its S^T of
+        // tile n_w - 1 is the first needed), the masked tiles [fm_w, n_w), the
+        // whole tiles, and the iteration after tile 0.
+        const int a = max(0, nt - n_w - 1);
+        phase(iteration, 0, a, idle);
+        phase(iteration, a, nt - fm_w, masked);
+        phase(iteration, nt - fm_w, nt, whole);
+        phase(iteration, nt, nt + 1, masked);
+      } else {
+        phase(iteration, 0, fm_w, whole);
+        phase(iteration, max(fm_w, 0), n_w + 1, masked);
+        phase(iteration, n_w + 1, nt + 1, idle);
+      }
+      // The scores of the last iterations are dead, but are kept live past
+      // the padding so that their registers are not reused while the MFMAs
+      // writing them are in flight.
+      hazard_pad();
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) keep_live(sc[pb].s[rb]);
     } else {
-      phase(0, fm_w, whole);
-      phase(max(fm_w, 0), n_w + 1, masked);
-      phase(n_w + 1, nt + 1, idle);
-    }
-
-    // The next item's K/V copies go out before this item's output is
-    // written, so that their latencies overlap.
-    Item nxt;
-    const bool more = item_at(round + 1, nxt);
-    if (more) start_item(nxt);
-
-    // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
-    // head dims 32 db + 8 g + 4 hh + 0..3 of its row; they go to the wave's
-    // staging region in the K-tile layout, come back as whole 16-byte chunks
-    // (1 KB of consecutive rows per instruction) and are stored from there,
-    // rows past Lq falling outside the store's range.  The scores of the last
-    // iteration are dead, but are kept live past the padding so that their
-    // registers are not reused while the MFMAs writing them are in flight.
-    hazard_pad();
+      // ---- P.V wave: O^T += V^T P^T of tile j-1, and the HBM -> LDS copies ----
+      Addr ad;
+      PF::make_addr_v(ad, lane);
+      // Global offsets of this lane's HBM -> LDS copies (copying wave cw =
+      // pair): in copy u the lane writes bytes 16 lane .. 16 lane + 15 of 1 KB
+      // block u * kCopyWaves + cw, i.e. chunk position lane % CPR of row
+      // (block * 1024 / (2 D) + lane / CPR), and reads the global chunk that
+      // the swizzle puts there.
+      const int cw = pair;
+      int dof[NI];
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) keep_live(sc[pb].s[rb]);
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const float lt = sum_halves(rb == 0 ? agpr_read<kLAgpr>() : agpr_read<kLAgpr + 4>());
-      const float inv = lt > 0.f ? 1.f / lt : 0.f;
-      st.alpha[rb] = inv;
-    }
-    static_for<RB * PF::DB * 4>([&](auto ic) {
-      constexpr int f = decltype(ic)::value;
-      constexpr int rb = f / (PF::DB * 4), db = (f / 4) % PF::DB, g = f % 4;
-      constexpr int a0 = PF::oagpr(rb, db) + 4 * g;
-      const float inv = st.alpha[rb];
-      uint2 w;
-      w.x = PF::E::pack2(agpr_read<a0>() * inv, agpr_read<a0 + 1>() * inv);
-      w.y = PF::E::pack2(agpr_read<a0 + 2>() * inv, agpr_read<a0 + 3>() * inv);
-      const int r = 32 * rb + n;
-      *reinterpret_cast<uint2*>(qo + r * D + 8 * ((4 * db + g) ^ swz<D>(r)) + 4 * hh) = w;
-    });
-    {
-      constexpr int NB = RB * TE * (int)sizeof(T) / 1024;
-      const int left = max(min(Lq - iw, RB * 32), 0) * D * (int)sizeof(T);
-      const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
-          reinterpret_cast<T*>(p.o) + ((size_t)cur.head * Lq + iw) * D, 0, left, 0x00020000);
-      const char* qob = reinterpret_cast<const char*>(qo);
-#pragma unroll
-      for (int blk = 0; blk < NB; ++blk) {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(qob + blk * 1024 + lane * 16);
+      for (int u = 0; u < NI; ++u) {
+        const int blk = u * kCopyWaves + cw;
         const int r = blk * (1024 / (2 * D)) + lane / CPR;
         const int pos = lane % CPR;
-        __builtin_amdgcn_raw_buffer_store_b128(w, orsrc, (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T), 0, 0);
+        dof[u] = (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T);
       }
+      auto copy_tile = [&](const T* base, uint32_t slot, int j) __attribute__((always_inline)) {
+        PF::copy_tile(base, slot, tile(j), cur.rows, cw, dof);
+      };
+      // The V slots of iterations -1 and -2 zeroed (nothing multiplies them:
+      // the first P.V iterations are idle, but a zero tile keeps the ring
+      // free of stale non-finite values), the copies of the K tiles of
+      // iterations 0 .. kRing-2 and of the V tile of iteration 0 issued.
+      {
+        constexpr int NV16 = TE * (int)sizeof(T) / 16;
+        uint4* vz = reinterpret_cast<uint4*>(lds + (kRing + kRing - 2) * TE);   // slots kRing-2, kRing-1
+#pragma unroll
+        for (int i = tid - kPairs * 64; i < 2 * NV16; i += kPairs * 64) vz[i] = make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < kRing - 1; ++j) copy_tile(kp, kslot(j), j);
+      copy_tile(vp, vslot(0), 0);
+      static_for<RB * DB * 16>([&](auto ic) { agpr_zero<PF::oagpr(0, 0) + decltype(ic)::value>(); });
+      static_for<RB * 4>([&](auto ic) { agpr_zero<kLAgpr + decltype(ic)::value>(); });
+      agpr_write<kOnesAgpr>(PF::M::kOnes);
+      agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
+      typename PF::template Ring<false> fr;
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      // The first fragments of iteration -1: the zeroed V slot of tile -2.
+      PF::template prime<false>(fr, lds + (kRing + kRing - 2) * TE, ad);
+      // Iteration j: copies of K_{j+kRing} and V_{j+kRing-2}; with VAR 1, P and
+      // the rescale factors of tile j-1 from the exchange buffer of parity
+      // j-1, the rescale of O^T and l when some factor differs from 1, then
+      // P.V of tile j-1 from the V slot (j-1) mod kRing.  A tile's first
+      // fragments are read at the end of the iteration before its use, so
+      // its copy, issued kRing - 1 iterations before its use into the slot
+      // read by the iteration before, must be complete at the barrier that
+      // ends the iteration two before its use: vmcnt lets only the current
+      // iteration's copies stay in flight (every iteration issues the same
+      // number of copies), and lgkmcnt lets the reads of the next
+      // iteration's first fragments, which touch neither slot copied into
+      // next, cross the barrier.
+      auto iteration = [&](int j, auto var, auto slotc) __attribute__((always_inline)) {
+        constexpr int VAR = decltype(var)::value;
+        constexpr int k = decltype(slotc)::value;   // j mod kRing
+        constexpr int par = (k + 1) & 1;            // parity of j - 1
+        copy_tile(kp, kslot(k), j + kRing);
+        copy_tile(vp, vslot((k + kRing - 2) % kRing), j + kRing - 2);
+        const T* vl_use = lds + (kRing + (k + kRing - 1) % kRing) * TE;  // V_{j-1}
+        const T* vl_nxt = lds + (kRing + k) * TE;                        // V_j
+        if constexpr (VAR != 0) {
+          Probs pr;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int cc = 0; cc < 2; ++cc) {
+              const u32x4 w = xch[pair][par][rb * 2 + cc][lane];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) pr.w[rb][cc][e] = w[e];
+            }
+          const u32x4 a = xch[pair][par][2 * RB][lane];
+          const float alpha[RB] = {as_f(a[0]), as_f(a[1])};
+          if (__builtin_amdgcn_ballot_w64(alpha[0] != 1.f || alpha[1] != 1.f) != 0) PF::repair(alpha);
+          PF::iterate_o(pr, fr, vl_use, vl_nxt, ad);
+        } else {
+          PF::template prime<false>(fr, vl_nxt, ad);
+        }
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_waitcnt vmcnt(%0) lgkmcnt(%1)\n\ts_barrier"
+                     : : "n"(2 * NI), "n"(PF::kPrimeV) : "memory");
+      };
+      iteration(-1, idle, std::integral_constant<int, kRing - 1>{});
+      if constexpr (REV) {
+        // P.V of tile(j-1) = nt - j is needed for nt - n_w < j <= nt.
+        phase(iteration, 0, nt - n_w + 1, idle);
+        phase(iteration, nt - n_w + 1, nt + 1, whole);
+      } else {
+        // P.V of tile j-1 is needed for 1 <= j <= n_w.
+        phase(iteration, 0, 1, idle);
+        phase(iteration, 1, n_w + 1, whole);
+        phase(iteration, n_w + 1, nt + 1, idle);
+      }
+
+      // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
+      // head dims 32 db + 8 g + 4 hh + 0..3 of its row.
+      hazard_pad();
+      float inv[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const float lt = sum_halves(rb == 0 ? agpr_read<kLAgpr>() : agpr_read<kLAgpr + 4>());
+        inv[rb] = lt > 0.f ? 1.f / lt : 0.f;
+      }
+      static_for<RB * DB * 4>([&](auto ic) {
+        constexpr int f = decltype(ic)::value;
+        constexpr int rb = f / (DB * 4), db = (f / 4) % DB, g = f % 4;
+        constexpr int a0 = PF::oagpr(rb, db) + 4 * g;
+        uint2 w;
+        w.x = PF::E::pack2(agpr_read<a0>() * inv[rb], agpr_read<a0 + 1>() * inv[rb]);
+        w.y = PF::E::pack2(agpr_read<a0 + 2>() * inv[rb], agpr_read<a0 + 3>() * inv[rb]);
+        const int row = row0 + 32 * rb;
+        if (row < Lq) {
+          T* op = reinterpret_cast<T*>(p.o) + ((size_t)cur.head * Lq + row) * D;
+          *reinterpret_cast<uint2*>(op + 32 * db + 8 * g + 4 * hh) = w;
+        }
+      });
     }
-    // The region is free once its reads have returned: the next item's Q.
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    if (more) copy_q(nxt);
-    if (!more) break;
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    Item nxt;
+    if (!item_at(round + 1, nxt)) break;
     cur = nxt;
   }
 }
