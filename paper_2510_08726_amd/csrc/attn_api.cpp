@@ -15,8 +15,9 @@ thread_local int g_last_hip_error = 0;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int64_t kMaxGrid = std::numeric_limits<int32_t>::max();
-constexpr int kMinChunk = 256;    // keys per decode chunk chosen by the heuristic
-constexpr int kTargetBlocks = 4096;
+constexpr int kMinChunk = 256;    // keys per decode chunk chosen by the heuristic (one head per KV head)
+constexpr int kTargetBlocks = 8192;
+constexpr int kMinChunkGrouped = 128;   // grouped heads: at least one 32-key tile per wave
 
 bool shape_ok(int B, int Hq, int Hkv, int Lq, int Lk) {
   return B >= 1 && Hq >= 1 && Hkv >= 1 && Lq >= 1 && Lk >= 1 && Hq % Hkv == 0;
@@ -36,6 +37,17 @@ bool sizes_fit(int B, int Hq, int Hkv, int Lq, int Lk, int D) {
 int hip_fail(hipError_t e) {
   g_last_hip_error = (int)e;
   return ATTN_ERR_HIP;
+}
+
+// Compute units of the current device (the grouped decode kernel wants one
+// workgroup per compute unit: each holds 128 KB of LDS, so more would run one
+// after another, each paying its start-up and merge again).
+int compute_units() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n <= 0)
+    n = 256;
+  return n;
 }
 
 int gqa_heads_per_block(int group) {
@@ -99,6 +111,16 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
 
 int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D) {
   if (!shape_ok(B, Hq, Hkv, 1, Lk) || (D != 64 && D != 128)) return 0;
+  const int group = Hq / Hkv;
+  if (group >= 2 && group <= 32) {
+    // The grouped kernel: one workgroup per (chunk, KV head, batch).
+    const int64_t units = (int64_t)B * Hkv;
+    int64_t s = (compute_units() + units - 1) / units;
+    const int64_t smax = ((int64_t)Lk + kMinChunkGrouped - 1) / kMinChunkGrouped;
+    if (s > smax) s = smax;
+    if (s < 1) s = 1;
+    return (int)s;
+  }
   const int64_t groups = Hq / Hkv / gqa_heads_per_block(Hq / Hkv);
   const int64_t units = (int64_t)B * Hkv * groups;
   int64_t s = (kTargetBlocks + units - 1) / units;

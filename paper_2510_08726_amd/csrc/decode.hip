@@ -209,6 +209,238 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
   }
 }
 
+// Grouped-query decode on the matrix unit.  One workgroup per (chunk s, key/
+// value head, batch) serves all G = Hq / Hkv query heads of the key/value
+// head (G <= 32).  The heads are the N columns of 32x32x16 MFMAs:
+//   S^T = K . Q^T     (32 keys x G heads per tile; columns >= G hold zero Q)
+//   O^T += V^T . P^T  (head dims x G heads)
+// so the per-key work left on the VALU is the softmax of 16 keys per lane.
+// The chunk is split into four contiguous key ranges, one per wave; each wave
+// streams its keys in 32-key tiles into a wave-private, double-buffered LDS
+// region with buffer loads that write LDS directly (K and V tiles in the
+// swizzled row-major layout, K read back as operand fragments, V through the
+// transposing LDS read), and keeps an online-softmax state per head column.
+// The four waves' states are merged at the end into the same partials as the
+// vector kernel writes.  P is rounded to the input type as the MFMA operand
+// (the compute definition casts exp to the input type before the second
+// matmul), while the chunk's exp-sum l is accumulated from the fp32 values,
+// as that definition sums them.
+template <int D, typename T, bool ALIBI>
+__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
+  typedef Elem<T> E;
+  typedef typename E::vec8 vec8;
+  constexpr int KX = D / 16;                 // MFMA K-steps of K.Q^T
+  constexpr int DB = D / 32;                 // 32-dim blocks of O^T
+  constexpr int TN = 32;                     // keys per tile
+  constexpr int TB = TN * D * (int)sizeof(T);  // bytes of a K or V tile
+  constexpr int NBLK = TB / 1024;            // 1 KB copies per tile
+  constexpr int CPR = D / 8;                 // 16-byte chunks per row
+  // LDS: per wave, two buffers of (K tile, V tile).  After the key loop the
+  // same memory holds the merge: o [4][32][D] floats, then m and l [4][32].
+  constexpr int kLdsBytes = 4 * 2 * 2 * TB;
+  static_assert(4 * 32 * D * 4 + 2 * 4 * 32 * 4 <= kLdsBytes, "merge fits the tile buffers");
+  __shared__ __attribute__((aligned(1024))) char lds[kLdsBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 31, hh = lane >> 5;
+
+  const int S = p.splits;
+  const int G = p.group;
+  int bid = blockIdx.x;
+  const int s = bid % S;  bid /= S;
+  const int hk = bid % p.Hkv;
+  const int b = bid / p.Hkv;
+  const int hq0 = hk * G;
+  const int Lk = p.Lk;
+  const int ks = min(s * p.chunk, Lk);
+  const int ke = min(ks + p.chunk, Lk);
+  const int per = (ke - ks + 4 * TN - 1) / (4 * TN) * TN;   // keys per wave, whole tiles
+  const int kw0 = min(ks + wave * per, ke);
+  const int kw1 = min(kw0 + per, ke);
+  const int ntile = (kw1 - kw0 + TN - 1) / TN;
+
+  const T* kbase = reinterpret_cast<const T*>(p.k) + (size_t)(b * p.Hkv + hk) * Lk * D;
+  const T* vbase = reinterpret_cast<const T*>(p.v) + (size_t)(b * p.Hkv + hk) * Lk * D;
+  char* const wl = lds + wave * 2 * 2 * TB;                 // this wave's buffers
+  const uint32_t wl_addr = (uint32_t)(uintptr_t)(lds_void*)wl;
+
+  // Copy of tile t (keys kw0 + 32 t ..) into buffer bf: block blk of a tile
+  // holds rows blk * 1024 / (2 D) + lane / CPR, chunk position lane % CPR,
+  // filled from the global chunk the swizzle puts there; keys at or past kw1
+  // read as zero.
+  int goff[NBLK];
+#pragma unroll
+  for (int blk = 0; blk < NBLK; ++blk) {
+    const int r = blk * (1024 / (2 * D)) + lane / CPR;
+    const int pos = lane % CPR;
+    goff[blk] = (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T);
+  }
+  auto copy_tile = [&](int t, int bf) __attribute__((always_inline)) {
+    const int k0 = kw0 + TN * t;
+    const int left = max(kw1 - k0, 0) * D * (int)sizeof(T);
+#pragma unroll
+    for (int kv = 0; kv < 2; ++kv) {
+      const uint64_t a = reinterpret_cast<uint64_t>((kv == 0 ? kbase : vbase) + (size_t)k0 * D);
+      const u32x4 rsrc = {(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
+                          (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
+                          (uint32_t)__builtin_amdgcn_readfirstlane(left), 0x00020000u};
+      const uint32_t dst = wl_addr + (uint32_t)((bf * 2 + kv) * TB);
+#pragma unroll
+      for (int blk = 0; blk < NBLK; ++blk)
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                     : : "s"(dst + (uint32_t)(blk * 1024)), "v"(goff[blk]), "s"(rsrc) : "memory", "m0");
+    }
+  };
+
+  // Per-lane LDS offsets: K fragment kx (lane (n, hh): key n, dims 16 kx +
+  // 8 hh .. + 7) and V^T fragment (c16, db) (see the prefill kernel).
+  int ak[KX], av[DB][2];
+#pragma unroll
+  for (int kx = 0; kx < KX; ++kx) ak[kx] = 2 * (n * D + 8 * ((2 * kx + hh) ^ swz<D>(n)));
+  {
+    const int Gq = lane >> 4, i = lane & 15;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int lh = 0; lh < 2; ++lh) {
+        const int d = 32 * db + 16 * (Gq & 1) + 4 * (i & 3);
+        const int k = 4 * (Gq >> 1) + (i >> 2) + 8 * lh;
+        av[db][lh] = 2 * (k * D + 8 * ((d >> 3) ^ swz<D>(k)) + (d & 7));
+      }
+  }
+
+  // Q^T as the B operand: lane (n, hh) holds Q[head hq0 + n][16 kx + 8 hh ..]
+  // for n < G, zero otherwise.
+  vec8 qf[KX];
+  {
+    const T* qp = reinterpret_cast<const T*>(p.q) + ((size_t)b * p.Hq + hq0 + n) * D;
+#pragma unroll
+    for (int kx = 0; kx < KX; ++kx) {
+      u32x4 w = {0u, 0u, 0u, 0u};
+      if (n < G) w = *reinterpret_cast<const u32x4*>(qp + 16 * kx + 8 * hh);
+      qf[kx] = __builtin_bit_cast(vec8, w);
+    }
+  }
+  const float c = p.c;
+  const float sl2 = (ALIBI && n < G) ? p.slopes[hq0 + n] * kLog2e : 0.f;
+
+  float m = kNegInf, l = 0.f;      // log2 units; l: this lane's half of the keys
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[db] = f32x16{};
+
+  if (ntile > 0) copy_tile(0, 0);
+  if (ntile > 1) copy_tile(1, 1);
+  for (int t = 0; t < ntile; ++t) {
+    const int bf = t & 1;
+    if (t + 1 < ntile) asm volatile("s_waitcnt vmcnt(%0)" : : "n"(2 * NBLK) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const char* kt = wl + (bf * 2) * TB;
+    const char* vt = wl + (bf * 2 + 1) * TB;
+
+    f32x16 sacc = f32x16{};
+#pragma unroll
+    for (int kx = 0; kx < KX; ++kx) {
+      const vec8 kf = __builtin_bit_cast(vec8, *reinterpret_cast<const u32x4*>(kt + ak[kx]));
+      sacc = E::mfma(kf, qf[kx], sacc);
+    }
+    // Register r of lane (n, hh) is key 8 (r / 4) + 4 hh + r % 4 of the tile,
+    // head column n.
+    const int k0 = kw0 + TN * t;
+    float x[16];
+    float tmax = kNegInf;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = k0 + 8 * (r / 4) + 4 * hh + (r % 4);
+      float v = sacc[r] * c;
+      if (ALIBI) v = __builtin_fmaf(sl2, (float)(key - (Lk - 1)), v);
+      x[r] = key < kw1 ? v : kNegInf;
+      tmax = fmaxf(tmax, x[r]);
+    }
+    tmax = fmaxf(tmax, swap_halves(tmax));
+    const float mnew = fmaxf(m, tmax);
+    const float alpha = (m == kNegInf) ? 0.f : fast_exp2(m - mnew);
+    uint32_t w[2][4];
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) {
+      const float p0 = x[r] == kNegInf ? 0.f : fast_exp2(x[r] - mnew);
+      const float p1 = x[r + 1] == kNegInf ? 0.f : fast_exp2(x[r + 1] - mnew);
+      w[r / 8][(r % 8) / 2] = E::pack2(p0, p1);
+      ps += p0 + p1;
+    }
+    if (mnew != kNegInf) {
+      m = mnew;
+      l = __builtin_fmaf(l, alpha, ps);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] *= alpha;
+    }
+#pragma unroll
+    for (int c16 = 0; c16 < 2; ++c16) {
+      const vec8 pb = __builtin_bit_cast(vec8, make_uint4(w[c16][0], w[c16][1], w[c16][2], w[c16][3]));
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const char* base = vt + c16 * 32 * D;
+        const uint2 lo = lds_read_tr(base + av[db][0]);
+        const uint2 hi = lds_read_tr(base + av[db][1]);
+        const vec8 vf = __builtin_bit_cast(vec8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        o[db] = E::mfma(vf, pb, o[db]);
+      }
+    }
+    // Buffer bf is free once this tile's reads have returned.
+    if (t + 2 < ntile) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      copy_tile(t + 2, bf);
+    }
+  }
+
+  // Merge the four waves through LDS (the tile buffers are free after the
+  // barrier).  Lane (n, hh) holds O^T[32 db + 8 i + 4 hh + j][head n] in
+  // register 4 i + j of block db.
+  __syncthreads();
+  float* sh_o = reinterpret_cast<float*>(lds);               // [4][32][D]
+  float* sh_m = sh_o + 4 * 32 * D;                           // [4][32]
+  float* sh_l = sh_m + 4 * 32;                               // [4][32]
+  const float lt = l + swap_halves(l);
+  if (n < G) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sh_o[(wave * 32 + n) * D + 32 * db + 8 * (r / 4) + 4 * hh + (r % 4)] = o[db][r];
+    if (hh == 0) {
+      sh_m[wave * 32 + n] = m;
+      sh_l[wave * 32 + n] = lt;
+    }
+  }
+  __syncthreads();
+  const size_t rowbase = (size_t)b * p.Hq + hq0;
+  for (int idx = tid; idx < G * D; idx += kThreads) {
+    const int g = idx / D, d = idx % D;
+    float M = kNegInf;
+#pragma unroll
+    for (int wv = 0; wv < 4; ++wv) M = fmaxf(M, sh_m[wv * 32 + g]);
+    float L = 0.f, acc = 0.f;
+    if (M != kNegInf) {
+#pragma unroll
+      for (int wv = 0; wv < 4; ++wv) {
+        const float mw = sh_m[wv * 32 + g];
+        const float f = mw == kNegInf ? 0.f : fast_exp2(mw - M);
+        L = __builtin_fmaf(sh_l[wv * 32 + g], f, L);
+        acc = __builtin_fmaf(sh_o[(wv * 32 + g) * D + d], f, acc);
+      }
+    }
+    const size_t slot = (rowbase + g) * S + s;
+    p.ws_o[slot * D + d] = acc;
+    if (d == 0) {
+      p.ws_m[slot] = M == kNegInf ? kNegInf : M * kLn2;   // natural-log units
+      p.ws_l[slot] = L;
+    }
+  }
+}
+
 // Global nests: one workgroup per (batch, query head), one thread per head
 // dim.  Pass 1 takes max_g over all chunk maxima (a block reduction); pass 2
 // computes each chunk's weight exp(max_l - max_g) once into LDS, in batches,
@@ -283,7 +515,23 @@ hipError_t launch_split(const DecodeParams& p, hipStream_t stream) {
 }
 
 template <int D, typename T>
+hipError_t launch_mfma(const DecodeParams& p, hipStream_t stream) {
+  const int nblocks = p.splits * p.Hkv * p.B;
+  if (p.slopes)
+    hipLaunchKernelGGL((decode_mfma_kernel<D, T, true>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL((decode_mfma_kernel<D, T, false>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((decode_combine_kernel<D, T>), dim3(p.B * p.Hq), dim3(D), 0, stream, p);
+  return hipGetLastError();
+}
+
+// Grouped heads (2 <= G <= 32) go to the matrix-unit kernel; single heads to
+// the vector kernel, whose lane groups stream key rows with nothing wasted.
+template <int D, typename T>
 hipError_t launch_g(const DecodeParams& p, hipStream_t stream) {
+  if (p.group >= 2 && p.group <= 32) return launch_mfma<D, T>(p, stream);
   if (p.group % 8 == 0) return launch_split<D, T, 8>(p, stream);
   if (p.group % 4 == 0) return launch_split<D, T, 4>(p, stream);
   if (p.group % 2 == 0) return launch_split<D, T, 2>(p, stream);

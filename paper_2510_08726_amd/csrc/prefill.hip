@@ -89,30 +89,6 @@ constexpr float kMcInit = -1e30f;
 // launch are dealt to them in turn.
 constexpr int kXcds = 8;
 
-// K and V tiles live in LDS row-major, [BN][D], with the 16-byte chunks of
-// each row XOR-swizzled: chunk c of row r sits at chunk position c ^ swz(r).
-// That keeps the K operand reads (16 consecutive rows at one chunk) and the
-// transposing V reads (4 consecutive rows x 4 consecutive chunks per
-// half-wave) free of bank conflicts; the copy engine writes whole 1 KB
-// blocks, so the swizzle is applied on the global side of the copy.
-// swz depends on r % 16 only.
-template <int D>
-__device__ __forceinline__ int swz(int r) {
-  if (D == 128) return 4 * (r & 3) + ((r >> 2) & 3);
-  return 4 * ((r >> 1) & 1) + ((r >> 2) & 3);
-}
-
-typedef short v4s __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4s lds_v4s;
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Transposing LDS read: within each 16-lane group, output lane i element j is
-// element (i % 4) of the 8 bytes addressed by lane (i / 4 + 4 j).
-__device__ __forceinline__ uint2 lds_read_tr(const void* p) {
-  v4s r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p));
-  return __builtin_bit_cast(uint2, r);
-}
-
 __device__ __forceinline__ float as_f(unsigned u) { return __builtin_bit_cast(float, u); }
 __device__ __forceinline__ unsigned as_u(float f) { return __builtin_bit_cast(unsigned, f); }
 

@@ -49,14 +49,14 @@ WORKLOADS = {
     "causal_mha_prefill": Workload("causal_mha_prefill", 4, 32, 32, 2048, 2048,
                                    128, "f16", causal=True, seed=2),
     "mha_decode": Workload("mha_decode", 8, 32, 32, 1, 8192, 128, "f16",
-                           decode=True, seed=3, num_splits=32),
+                           decode=True, seed=3),
     "gqa_causal_prefill": Workload("gqa_causal_prefill", 2, 64, 8, 4096, 4096,
                                    128, "bf16", causal=True, seed=4),
     "alibi_causal_prefill": Workload("alibi_causal_prefill", 4, 16, 16, 4096,
                                      4096, 64, "f16", causal=True, alibi=True,
                                      seed=5),
     "gqa_long_decode": Workload("gqa_long_decode", 16, 32, 8, 1, 32768, 128,
-                                "f16", decode=True, seed=6, num_splits=32),
+                                "f16", decode=True, seed=6),
 }
 
 

@@ -104,14 +104,20 @@ def test_workspace_check_uses_resolved_split_count(lib):
 
 
 def test_num_splits_heuristic(lib):
+    # One query head per KV head: about 4096 workgroups, chunks of >= 256 keys.
     assert pa.attn_decode_num_splits(8, 32, 32, 8192, 128) >= 16
-    assert pa.attn_decode_num_splits(16, 32, 8, 32768, 128) >= 16
     assert pa.attn_decode_num_splits(1, 1, 1, 1, 64) == 1
     assert pa.attn_decode_num_splits(1, 1, 1, 300, 64) == 2    # chunks of >= 256 keys
     assert pa.attn_decode_num_splits(0, 1, 1, 300, 64) == 0
-    for B, Hq, Hkv, Lk in [(1, 4, 2, 777), (4, 16, 16, 5000), (2, 64, 8, 100000)]:
+    # 2..32 query heads per KV head: one workgroup per (chunk, KV head, batch),
+    # about one per compute unit (256 on MI355X, also the fallback without a
+    # device), chunks of >= 128 keys.
+    assert pa.attn_decode_num_splits(16, 32, 8, 32768, 128) == 2
+    assert pa.attn_decode_num_splits(1, 4, 2, 200, 128) == 2    # chunks of >= 128 keys
+    for B, Hq, Hkv, Lk in [(1, 4, 2, 777), (4, 16, 16, 5000), (2, 64, 8, 100000), (1, 64, 1, 5000)]:
         S = pa.attn_decode_num_splits(B, Hq, Hkv, Lk, 128)
-        assert 1 <= S <= -(-Lk // 256)
+        grouped = 2 <= Hq // Hkv <= 32
+        assert 1 <= S <= -(-Lk // (128 if grouped else 256))
 
 
 def test_binding_rejects_cpu_tensors():

@@ -43,6 +43,8 @@ CASES = [  # B, Hq, Hkv, Lk, D, dtype, S, alibi
     (1, 2, 2, 1, 64, "f16", 4, False),         # one key, three empty chunks
     (1, 32, 4, 2500, 128, "bf16", 100, False),
     (2, 16, 1, 3000, 64, "bf16", 7, True),     # 16 query heads per KV head
+    (1, 32, 1, 700, 128, "f16", 3, True),      # 32 query heads per KV head: every MFMA column
+    (2, 4, 2, 515, 64, "bf16", 2, True),       # 2 query heads per KV head, D 64
 ]
 
 
@@ -68,8 +70,14 @@ def test_decode_matches_oracle(case):
     live = ~empty
     np.testing.assert_allclose(m_l[live], rm[live], atol=1e-4, rtol=1e-5)
     np.testing.assert_allclose(s_l[live], rs[live], rtol=2e-4)
+    # The chunk-normalised partial is a weighted mean of V rows.  The weights
+    # that multiply V are rounded to the input type (the compute definition
+    # casts exp before the second matmul), a relative error of up to 2^-11
+    # (fp16) or 2^-9 (bf16) per weight, so a chunk of few keys can be off by
+    # about that times max |V| (~4 for N(0,1) rows).
+    tol = 2e-3 if dt == "f16" else 8e-3
     np.testing.assert_allclose((o_l / np.where(live, s_l, 1)[..., None])[live],
-                               (ro / np.where(live, rs, 1)[..., None])[live], atol=2e-3)
+                               (ro / np.where(live, rs, 1)[..., None])[live], atol=tol)
 
 
 def test_decode_independent_of_split_count_and_equals_prefill_row():
