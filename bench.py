@@ -10,9 +10,10 @@ inputs are resident in HBM before the timed region.
 
 The headline line is the causal MHA prefill workload (B=4, H=32, L=2048,
 D=128, fp16): `value` is its algorithmic TFLOP/s (4*D per visible query/key
-pair).  The decode workload (B=8, H=32, Lk=8192, D=128) is reported beside it
-in `decode` as algorithmic GB/s (|Q|+|K|+|V|+|O|), and every workload is listed
-under `workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
+pair).  The decode workloads (B=8, H=32, Lk=8192, D=128; and B=16, Hq=32,
+Hkv=8, Lk=32768, D=128) are reported beside it in `decode` and `decode_gqa` as
+algorithmic GB/s (|Q|+|K|+|V|+|O|), and every workload is listed under
+`workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
 bounded sample of the headline workload.
 """
 
@@ -30,6 +31,7 @@ MFMA_PEAK_TFLOPS = 2500.0    # MI355X dense fp16/bf16 MFMA, published
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 HEADLINE = "causal_mha_prefill"
 DECODE_HEADLINE = "mha_decode"
+DECODE_GQA = "gqa_long_decode"
 METRIC = "prefill attn TFLOP/s (% MFMA peak); decode KV-read GB/s (% HBM peak)"
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
@@ -58,6 +60,19 @@ def measured_traffic(kind, workload):
     if not ent or ent.get("source_hash") != kernel_source_hash(kind):
         return None
     return ent.get("traffic_bytes_per_step")
+
+
+def decode_entry(name, dec):
+    """The decode workload's throughput and its HBM roofline (split + combine kernels)."""
+    return {
+        "workload": name, "value": dec["GB/s"], "unit": "GB/s",
+        "ms_per_step": dec["ms_per_step"], "num_splits": dec["num_splits"],
+        "roofline": {"bound": "hbm", "achieved": dec["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(dec["GB/s"] / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("decode", name),
+                     "per_launch": f"{dec['bytes_per_step']} algorithmic bytes (|Q|+|K|+|V|+|O|), "
+                                   "split + combine kernels"},
+    }
 
 
 def parse():
@@ -204,7 +219,6 @@ def main():
         print(f"# {name}: {json.dumps(results[name])}", file=sys.stderr, flush=True)
 
     head = results[HEADLINE]
-    dec = results[DECODE_HEADLINE]
     w = WORKLOADS[HEADLINE]
     traffic = measured_traffic("prefill", HEADLINE)
     roofline = {
@@ -213,15 +227,8 @@ def main():
         "kernel": "prefill_kernel<128, f16, causal>",
         "per_launch": f"{head['flops_per_step']} algorithmic flops (4*D per visible query/key pair)",
     }
-    dec_traffic = measured_traffic("decode", DECODE_HEADLINE)
-    decode = {
-        "workload": DECODE_HEADLINE, "value": dec["GB/s"], "unit": "GB/s",
-        "ms_per_step": dec["ms_per_step"], "num_splits": dec["num_splits"],
-        "roofline": {"bound": "hbm", "achieved": dec["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dec["GB/s"] / HBM_PEAK_GBS, 4), "traffic": dec_traffic,
-                     "per_launch": f"{dec['bytes_per_step']} algorithmic bytes (|Q|+|K|+|V|+|O|), "
-                                   "split + combine kernels"},
-    }
+    decode = decode_entry(DECODE_HEADLINE, results[DECODE_HEADLINE])
+    decode_gqa = decode_entry(DECODE_GQA, results[DECODE_GQA])
     line = {
         "metric": METRIC, "value": head["TFLOP/s"], "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
@@ -231,6 +238,7 @@ def main():
                    "D": w.D, "causal": w.causal, "input": "iid N(0,1) fp16, seed 2"},
         "roofline": roofline,
         "decode": decode,
+        "decode_gqa": decode_gqa,
         "workloads": results,
     }
     if not args.no_cpu_baseline:
