@@ -22,6 +22,7 @@ struct PrefillParams {
   int nheads;           // B * Hq, set by the launcher
   int nitems;           // nqb * nheads, set by the launcher
   int nxcd;             // XCDs the workgroups are spread over, set by the launcher
+  int hg;               // query heads per workgroup (sharing one KV head), set by the launcher
 };
 
 struct DecodeParams {

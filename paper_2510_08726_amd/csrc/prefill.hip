@@ -3,9 +3,12 @@
 // the plain attention definition, with the tile structure of the appendix
 // "Privatization" (a local max per key tile, then the running max).
 //
-// Work split.  One workgroup = 8 wave64s = 256 query rows of one (batch,
-// query head); two waves per SIMD, each owning 32 rows for the whole key
-// loop.  Key tiles are BN = 32 keys.  Every wave runs the whole loop body
+// Work split.  One workgroup = 8 wave64s, two per SIMD, each owning 32 query
+// rows of one query head for the whole key loop: 256 rows of one (batch,
+// query head), or, when several query heads share a KV head (GQA), the same
+// 256 / hg rows of hg such heads, so that every wave sees the same keys (no
+// wave idles while the others finish their causal diagonal) and all of them
+// read the same K and V tiles.  Key tiles are BN = 32 keys.  Every wave runs the whole loop body
 // for its rows, software-pipelined over three tiles: iteration j
 //
 //   S^T(j+1) = K_{j+1} . Q^T          8 (D = 128) 32x32x16 MFMAs, K from LDS,
@@ -65,7 +68,7 @@ namespace {
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int BMW = 32;                     // query rows per wave
-constexpr int BM = BMW * kWaves;            // query rows per workgroup
+constexpr int BM = BMW * kWaves;            // query rows per workgroup of one head
 constexpr int BN = 32;                      // keys per tile
 constexpr int kRing = 4;                    // LDS slots per operand; copies run kRing - 1 tiles ahead
 // A row's reference maximum moves only when a tile's maximum exceeds it by
@@ -569,10 +572,11 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     dof[u] = (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T);
   }
 
-  // Persistent workgroups.  The work items (query block, query head) are
-  // numbered KV head first, then query block by decreasing key count, then
-  // query head within the KV head's group, so that neighbouring items read
-  // the same K and V.  Workgroup g runs on XCD g mod kXcds (the order in
+  // Persistent workgroups.  The work items (query block, group of hg query
+  // heads) are numbered KV head first, then query block by decreasing key
+  // count, then head group within the KV head's group, so that neighbouring
+  // items read the same K and V.  Wave w takes head w mod hg of the group and
+  // row block w / hg of the query block.  Workgroup g runs on XCD g mod kXcds (the order in
   // which the dispatcher hands out the first workgroups), and each XCD takes
   // one contiguous share of the items, so the concurrent readers of a K/V
   // tile share that XCD's L2.  Within an XCD, round r gives item r * Pl + c
@@ -586,7 +590,10 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
   const int xcd = wg % X, c = wg / X, Pl = P / X;
   const int s0 = (int)((long long)p.nitems * xcd / X);
   const int s1 = (int)((long long)p.nitems * (xcd + 1) / X);
-  const int per_kv = p.nqb * p.group;
+  const int hg = p.hg;
+  const int ngrp = p.group / hg;              // head groups per KV head
+  const int bm = BMW * (kWaves / hg);         // query rows per work item
+  const int per_kv = p.nqb * ngrp;
   const int Lq = p.Lq, Lk = p.Lk;
   const int off = Lk - Lq;
 
@@ -602,14 +609,14 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     const int s = s0 + sl;
     it.kvh = s / per_kv;
     const int rem = s - it.kvh * per_kv;
-    it.qb = p.nqb - 1 - rem / p.group;
-    it.head = it.kvh * p.group + rem % p.group;
+    it.qb = p.nqb - 1 - rem / ngrp;
+    it.head = it.kvh * p.group + (rem % ngrp) * hg + wave % hg;
     it.hq = it.head % p.Hq;
-    const int i0 = it.qb * BM;
-    it.iw = i0 + BMW * wave;
+    const int i0 = it.qb * bm;
+    it.iw = i0 + BMW * (wave / hg);
     int kend = Lk, kend_w = Lk;
     if (CAUSAL) {
-      kend = min(Lk, min(i0 + BM, Lq) + off);
+      kend = min(Lk, min(i0 + bm, Lq) + off);
       kend_w = min(Lk, min(it.iw + BMW, Lq) + off);
     }
     if (it.iw >= Lq) kend_w = 0;
@@ -835,8 +842,14 @@ int compute_units() {
 template <int D, typename T, bool CAUSAL, bool ALIBI>
 hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
   PrefillParams q = p;
+  // Query heads per workgroup: the largest power of two (up to the wave
+  // count) that divides the GQA group.
+  q.hg = 1;
+  while (q.hg < kWaves && p.group % (2 * q.hg) == 0) q.hg *= 2;
+  const int bm = BMW * (kWaves / q.hg);
+  q.nqb = (p.Lq + bm - 1) / bm;
   q.nheads = p.B * p.Hq;
-  q.nitems = p.nqb * q.nheads;
+  q.nitems = q.nqb * (q.nheads / q.hg);
   if (q.nitems == 0) return hipSuccess;
   const int grid = std::min(q.nitems, compute_units());
   q.nxcd = grid % kXcds == 0 ? kXcds : 1;
