@@ -542,8 +542,10 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
   constexpr int NB = PF::NB;
   constexpr int CPW = PF::CPW;
   constexpr int CPR = PF::CPR;
-  // LDS: a ring of kRing K tiles, then a ring of kRing V tiles.
-  __shared__ __attribute__((aligned(1024))) T lds[2 * kRing * TE];
+  // LDS: a ring of kRing K tiles, a ring of kRing V tiles, then one tile
+  // per wave that stages the wave's 32 O rows out at the end of a work item,
+  // in the layout of the K and V tiles.
+  __shared__ __attribute__((aligned(1024))) T lds[(2 * kRing + kWaves) * TE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -802,10 +804,21 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     keep_live(sc[1]);
 
     // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
-    // head dims 32 db + 8 g + 4 hh + 0..3 of its row.
+    // head dims 32 db + 8 g + 4 hh + 0..3 of its row: it writes them to the
+    // wave's staging tile (chunk 4 db + g of the row, half hh; no other wave
+    // touches that tile), then the wave stores the tile row-major, 16 bytes a
+    // lane, whole rows per instruction.
     {
       const float lt = sum_halves(agpr_read<kLAgpr>());
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
+      char* xo = reinterpret_cast<char*>(lds + (2 * kRing + wave) * TE);
+      // The lane index passes through an opaque copy, so that the addresses
+      // below are computed here, once per work item, rather than hoisted out
+      // of the item loop into registers held through the key loop.
+      int ln = lane;
+      pin(ln);
+      const int n2 = ln & 31, h2 = ln >> 5;
+      const int sw = swz<D>(n2);
       static_for<DB * 4>([&](auto ic) {
         constexpr int f = decltype(ic)::value;
         constexpr int db = f / 4, g = f % 4;
@@ -813,10 +826,16 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
         uint2 w;
         w.x = PF::E::pack2(agpr_read<a0>() * inv, agpr_read<a0 + 1>() * inv);
         w.y = PF::E::pack2(agpr_read<a0 + 2>() * inv, agpr_read<a0 + 3>() * inv);
-        if (row < Lq) {
-          T* op = reinterpret_cast<T*>(p.o) + ((size_t)cur.head * Lq + row) * D;
-          *reinterpret_cast<uint2*>(op + 32 * db + 8 * g + 4 * hh) = w;
-        }
+        *reinterpret_cast<uint2*>(xo + 2 * (n2 * D + 8 * ((4 * db + g) ^ sw) + 4 * h2)) = w;
+      });
+      constexpr int RPI = 64 / CPR;   // rows per store instruction
+      const int pos = ln % CPR;
+      T* op = reinterpret_cast<T*>(p.o) + ((size_t)cur.head * Lq + iw) * D;
+      static_for<BMW / RPI>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        const int r = i * RPI + ln / CPR;
+        const uint4 w = *reinterpret_cast<const uint4*>(xo + 2 * (r * D + 8 * (pos ^ swz<D>(r))));
+        if (iw + r < Lq) *reinterpret_cast<uint4*>(op + (size_t)r * D + 8 * pos) = w;
       });
     }
 
