@@ -134,7 +134,8 @@ constexpr int kLAgpr = 96;      // exp-sum accumulator
 constexpr int kOnesAgpr = 100;  // two registers holding (1.0, 1.0)
 
 // 32x32x16 MFMAs.  qk0/qk: S^T accumulator in VGPRs (qk0 starts from zero), K
-// operand in VGPRs, Q operand from AGPRs a[QA .. QA + 3].  pv: O^T accumulator
+// operand in VGPRs, Q operand from AGPRs a[QA .. QA + 3]; with PAD, two wait
+// states first, for an operand that the compiler reloads (VALU) just before.  pv: O^T accumulator
 // a[OA .. OA + 15], both operands in VGPRs.  rowsum: a 4x4x4 MFMA with the
 // all-ones operand, which adds the four 16-bit values each lane holds in b to
 // every register of its accumulator a[LA .. LA + 3]: the exp-sum l is
@@ -143,11 +144,17 @@ constexpr int kOnesAgpr = 100;  // two registers holding (1.0, 1.0)
 template <typename T> struct Mma;
 template <> struct Mma<_Float16> {
   typedef f16x8 v8;
-  template <int QA> static __device__ __forceinline__ void qk0(f32x16& d, v8 a) {
-    asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  template <int QA, bool PAD> static __device__ __forceinline__ void qk0(f32x16& d, v8 a) {
+    if constexpr (PAD)
+      asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+    else
+      asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
   }
-  template <int QA> static __device__ __forceinline__ void qk(f32x16& d, v8 a) {
-    asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  template <int QA, bool PAD> static __device__ __forceinline__ void qk(f32x16& d, v8 a) {
+    if constexpr (PAD)
+      asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+    else
+      asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
   }
   template <int OA> static __device__ __forceinline__ void pv(v8 a, v8 b) {
     asm volatile("v_mfma_f32_32x32x16_f16 a[%2:%3], %0, %1, a[%2:%3]" : : "v"(a), "v"(b), "n"(OA), "n"(OA + 15) : ATTN_AGPRS);
@@ -160,11 +167,17 @@ template <> struct Mma<_Float16> {
 };
 template <> struct Mma<__bf16> {
   typedef bf16x8 v8;
-  template <int QA> static __device__ __forceinline__ void qk0(f32x16& d, v8 a) {
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  template <int QA, bool PAD> static __device__ __forceinline__ void qk0(f32x16& d, v8 a) {
+    if constexpr (PAD)
+      asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+    else
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], 0" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
   }
-  template <int QA> static __device__ __forceinline__ void qk(f32x16& d, v8 a) {
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  template <int QA, bool PAD> static __device__ __forceinline__ void qk(f32x16& d, v8 a) {
+    if constexpr (PAD)
+      asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+    else
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
   }
   template <int OA> static __device__ __forceinline__ void pv(v8 a, v8 b) {
     asm volatile("v_mfma_f32_32x32x16_bf16 a[%2:%3], %0, %1, a[%2:%3]" : : "v"(a), "v"(b), "n"(OA), "n"(OA + 15) : ATTN_AGPRS);
@@ -487,8 +500,11 @@ struct Prefill {
                 constexpr int f = i + PFD_K;
                 if constexpr (f < NG) read_frag<true, f>(fk, kl, ad);
                 else read_frag<true, f - NG>(fk, kln, ad);
-                if constexpr (i == 0) M::template qk0<qagpr(i)>(s_next, fk[i % (PFD_K + 1)]);
-                else M::template qk<qagpr(i)>(s_next, fk[i % (PFD_K + 1)]);
+                // Without the causal mask the kernel has the register
+                // pressure at which the compiler parks K operands in spare
+                // AGPRs and reloads them right before their MFMA.
+                if constexpr (i == 0) M::template qk0<qagpr(i), !CAUSAL>(s_next, fk[i % (PFD_K + 1)]);
+                else M::template qk<qagpr(i), !CAUSAL>(s_next, fk[i % (PFD_K + 1)]);
               }
             } else {
               if constexpr (PV) {
@@ -640,8 +656,50 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
   Addr ad;
   PF::make_addr(ad, lane);
 
+  // This wave's staging tile: Q rows in at the start of a work item, O rows
+  // out at its end.
+  const T* xl = lds + (2 * kRing + wave) * TE;
+  const uint32_t xslot = lds0 + (uint32_t)((2 * kRing + wave) * TE * (int)sizeof(T));
+  // The first tiles of a work item: K tiles 0 .. kRing-2 and V tile 0, each
+  // wave its blocks.  Issued once the previous item's last barrier has
+  // passed (every ring slot is free then), before that item's output.
+  auto stage_kv = [&](const Item& it) __attribute__((always_inline)) {
+    const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)it.kvh * Lk * D;
+    const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)it.kvh * Lk * D;
+#pragma unroll
+    for (int u = 0; u < CPW; ++u) {
+      const int b = (u * kWaves + wave) % NB;
+      if (PF::copies_k(u, wave)) {
+#pragma unroll
+        for (int t = 0; t < kRing - 1; ++t) PF::copy_block(kp, it.rows, kslot(t), tile_of(it, t), b, dof[u]);
+      } else {
+        PF::copy_block(vp, it.rows, vslot(0), tile_of(it, 0), b, dof[u]);
+      }
+    }
+  };
+  // The wave's 32 Q rows of a work item (rows past Lq read as zero) into its
+  // staging tile, as whole 1 KB blocks; issued after the wave has read its
+  // previous output out of that tile.  The lane index passes through an
+  // opaque copy so that the block offsets are computed here.
+  auto stage_q = [&](const Item& it) __attribute__((always_inline)) {
+    int ln = lane;
+    pin(ln);
+    const T* qp = reinterpret_cast<const T*>(p.q) + ((size_t)it.head * Lq + it.iw) * D;
+    const int qrows = max(min(Lq - it.iw, BMW), 0);
+    static_for<NB>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int r = b * (1024 / (2 * D)) + ln / CPR;
+      const int pos = ln % CPR;
+      PF::copy_block(qp, qrows, xslot, 0, b, (r * D + 8 * (pos ^ swz<D>(r))) * (int)sizeof(T));
+    });
+  };
+
   Item cur;
   if (!item_at(0, cur)) return;
+  agpr_write<kOnesAgpr>(PF::M::kOnes);
+  agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
+  stage_kv(cur);
+  stage_q(cur);
 
   for (int round = 0;; ++round) {
     const int nt = cur.nt, n_w = cur.n_w, fm_w = cur.fm_w;
@@ -674,37 +732,25 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
       }
     };
 
-    // Stage the first tiles: K tiles 0 .. kRing-2 and V tile 0 (each wave
-    // its blocks), Q into its AGPRs (B operand of S^T: lane (n, hh) holds
-    // Q[row][16 kx + 8 hh + 0..7]), negated for a negative scale; O^T and l
-    // zeroed.
-#pragma unroll
-    for (int u = 0; u < CPW; ++u) {
-      const int b = (u * kWaves + wave) % NB;
-      if (PF::copies_k(u, wave)) {
-#pragma unroll
-        for (int t = 0; t < kRing - 1; ++t) PF::copy_block(kp, cur.rows, kslot(t), tile(t), b, dof[u]);
-      } else {
-        PF::copy_block(vp, cur.rows, vslot(0), tile(0), b, dof[u]);
-      }
-    }
-    {
-      const T* qp = reinterpret_cast<const T*>(p.q) + (size_t)cur.head * Lq * D;
-      static_for<KX>([&](auto ic) {
-        constexpr int kx = decltype(ic)::value;
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (row < Lq) w = *reinterpret_cast<const u32x4*>(qp + (size_t)row * D + 16 * kx + 8 * hh);
-        agpr_write<PF::qagpr(kx) + 0>(w[0] ^ p.qsign);
-        agpr_write<PF::qagpr(kx) + 1>(w[1] ^ p.qsign);
-        agpr_write<PF::qagpr(kx) + 2>(w[2] ^ p.qsign);
-        agpr_write<PF::qagpr(kx) + 3>(w[3] ^ p.qsign);
-      });
-    }
+    // Q of this work item: from the wave's staging tile (copied in by
+    // stage_q) into its AGPRs, read like a K fragment (B operand of S^T: lane
+    // (n, hh) holds Q[row][16 kx + 8 hh + 0..7]), negated for a negative
+    // scale; O^T and l zeroed.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // (An opaque zero offset keeps the staging tile's per-fragment addresses
+    // from being hoisted out of the item loop.)
+    int zero = 0;
+    pin(zero);
+    static_for<KX>([&](auto ic) {
+      constexpr int kx = decltype(ic)::value;
+      const u32x4 w = __builtin_bit_cast(u32x4, PF::kfrag(xl + zero, ad, kx));
+      agpr_write<PF::qagpr(kx) + 0>(w[0] ^ p.qsign);
+      agpr_write<PF::qagpr(kx) + 1>(w[1] ^ p.qsign);
+      agpr_write<PF::qagpr(kx) + 2>(w[2] ^ p.qsign);
+      agpr_write<PF::qagpr(kx) + 3>(w[3] ^ p.qsign);
+    });
     static_for<DB * 16>([&](auto ic) { agpr_zero<kOAgpr + decltype(ic)::value>(); });
     static_for<4>([&](auto ic) { agpr_zero<kLAgpr + decltype(ic)::value>(); });
-    agpr_write<kOnesAgpr>(PF::M::kOnes);
-    agpr_write<kOnesAgpr + 1>(PF::M::kOnes);
-
     State st;
     st.mc = kMcInit;
     st.alpha = 1.f;
@@ -803,6 +849,10 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     keep_live(sc[0]);
     keep_live(sc[1]);
 
+    Item nxt;
+    const bool more = item_at(round + 1, nxt);
+    if (more) stage_kv(nxt);
+
     // Finalize: O = O^T / l, rounded to the input type.  Lane (n, hh) holds
     // head dims 32 db + 8 g + 4 hh + 0..3 of its row: it writes them to the
     // wave's staging tile (chunk 4 db + g of the row, half hh; no other wave
@@ -811,7 +861,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     {
       const float lt = sum_halves(agpr_read<kLAgpr>());
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
-      char* xo = reinterpret_cast<char*>(lds + (2 * kRing + wave) * TE);
+      char* xo = reinterpret_cast<char*>(const_cast<T*>(xl));
       // The lane index passes through an opaque copy, so that the addresses
       // below are computed here, once per work item, rather than hoisted out
       // of the item loop into registers held through the key loop.
@@ -839,8 +889,8 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
       });
     }
 
-    Item nxt;
-    if (!item_at(round + 1, nxt)) break;
+    if (!more) break;
+    stage_q(nxt);
     cur = nxt;
   }
 }
