@@ -265,10 +265,11 @@ struct Prefill {
   static constexpr int NS = 2 * NG;                        // MFMA slots per iteration
   static_assert(NG == 2 * DB, "as many V fragments as K fragments");
   static_assert(CPW >= 1 && 2 * NB == CPW * kWaves, "the copies of a tile divide evenly over the waves");
-  // K and V operand fragments read ahead of their MFMA.  With ALiBi (keys
-  // visited last to first, more live state) the V ring is shallower, which
-  // keeps the kernel inside its registers.
-  static constexpr int PFD_K = 3;
+  // K and V operand fragments read ahead of their MFMA (one K fragment is two
+  // MFMA slots).  With ALiBi (keys visited last to first, more live state)
+  // the V ring is shallower too.  Deeper K rings measured slower: the
+  // registers they hold push the per-item code into scratch.
+  static constexpr int PFD_K = 1;
   static constexpr int PFD_V = ALIBI ? 1 : 3;
   template <bool IS_K> static constexpr int pfd() { return IS_K ? PFD_K : PFD_V; }
   static_assert(NG % (PFD_K + 1) == 0 && NG % (PFD_V + 1) == 0, "fragment ring positions must repeat every iteration");
