@@ -12,7 +12,8 @@ The headline line is the causal MHA prefill workload (B=4, H=32, L=2048,
 D=128, fp16): `value` is its algorithmic TFLOP/s (4*D per visible query/key
 pair).  The decode workloads (B=8, H=32, Lk=8192, D=128; and B=16, Hq=32,
 Hkv=8, Lk=32768, D=128) are reported beside it in `decode` and `decode_gqa` as
-algorithmic GB/s (|Q|+|K|+|V|+|O|), and every workload is listed under
+algorithmic GB/s (|Q|+|K|+|V|+|O|), the ALiBi decode workload (the MHA decode
+shape with the ALiBi bias) in `decode_alibi`, and every workload is listed under
 `workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
 bounded sample of the headline workload.
 """
@@ -32,6 +33,7 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 HEADLINE = "causal_mha_prefill"
 DECODE_HEADLINE = "mha_decode"
 DECODE_GQA = "gqa_long_decode"
+DECODE_ALIBI = "alibi_decode"
 METRIC = "prefill attn TFLOP/s (% MFMA peak); decode KV-read GB/s (% HBM peak)"
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
@@ -229,6 +231,7 @@ def main():
     }
     decode = decode_entry(DECODE_HEADLINE, results[DECODE_HEADLINE])
     decode_gqa = decode_entry(DECODE_GQA, results[DECODE_GQA])
+    decode_alibi = decode_entry(DECODE_ALIBI, results[DECODE_ALIBI])
     line = {
         "metric": METRIC, "value": head["TFLOP/s"], "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
@@ -239,6 +242,7 @@ def main():
         "roofline": roofline,
         "decode": decode,
         "decode_gqa": decode_gqa,
+        "decode_alibi": decode_alibi,
         "workloads": results,
     }
     if not args.no_cpu_baseline:

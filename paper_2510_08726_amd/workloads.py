@@ -41,8 +41,9 @@ class Workload:
         return 1.0 / math.sqrt(self.D) if self.scale is None else self.scale
 
 
-# The six shapes the headline metric is quoted on.  Prefill: Lq == Lk.
-# Decode: one query token (Lq = 1) against a KV cache of Lk keys.
+# The six shapes the headline metric is quoted on, then ALiBi decode (the MHA
+# decode shape with the ALiBi bias).  Prefill: Lq == Lk.  Decode: one query
+# token (Lq = 1) against a KV cache of Lk keys.
 WORKLOADS = {
     "tiny_noncausal": Workload("tiny_noncausal", 1, 2, 2, 128, 128, 64, "f16",
                                seed=1),
@@ -57,6 +58,8 @@ WORKLOADS = {
                                      seed=5),
     "gqa_long_decode": Workload("gqa_long_decode", 16, 32, 8, 1, 32768, 128,
                                 "f16", decode=True, seed=6),
+    "alibi_decode": Workload("alibi_decode", 8, 32, 32, 1, 8192, 128, "f16",
+                             alibi=True, decode=True, seed=7),
 }
 
 

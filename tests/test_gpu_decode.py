@@ -108,7 +108,7 @@ def _workload_run(name):
     return w, q, k, v, sl, o.cpu()
 
 
-@pytest.mark.parametrize("name", ["mha_decode", "gqa_long_decode"])
+@pytest.mark.parametrize("name", ["mha_decode", "gqa_long_decode", "alibi_decode"])
 def test_decode_workload_full(name):
     """Every output row of the full-size decode workloads vs the oracle."""
     print(f"decode workload {name}", flush=True)
