@@ -37,6 +37,9 @@ CASES = [  # B, Hq, Hkv, Lq, Lk, D, dtype, causal, alibi
     (1, 2, 2, 1, 1, 64, "bf16", True, True),
     (1, 2, 2, 520, 520, 64, "f16", True, True),
     (1, 1, 1, 129, 1000, 128, "bf16", False, False),
+    (1, 16, 2, 300, 300, 128, "bf16", True, False),   # 8 query heads per KV head: one head per wave
+    (2, 8, 1, 70, 70, 64, "f16", True, True),         # 8 per KV head with ALiBi, a single ragged block
+    (1, 12, 3, 100, 260, 128, "f16", False, False),   # 4 query heads per KV head, Lk > Lq
 ]
 
 
