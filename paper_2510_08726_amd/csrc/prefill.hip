@@ -8,8 +8,9 @@
 // query head), or, when several query heads share a KV head (GQA), the same
 // 256 / hg rows of hg such heads, so that every wave sees the same keys (no
 // wave idles while the others finish their causal diagonal) and all of them
-// read the same K and V tiles.  Key tiles are BN = 32 keys.  Every wave runs the whole loop body
-// for its rows, software-pipelined over three tiles: iteration j
+// read the same K and V tiles.  Key tiles are BN = 32 keys.  Every wave runs
+// the whole loop body for its rows, software-pipelined over three tiles:
+// iteration j
 //
 //   S^T(j+1) = K_{j+1} . Q^T          8 (D = 128) 32x32x16 MFMAs, K from LDS,
 //                                      Q in AGPRs
@@ -37,7 +38,8 @@
 // The K and V tiles of the workgroup pass through LDS rings of kRing slots,
 // filled by buffer loads with the LDS bit (HBM -> LDS without VGPRs) that all
 // waves issue, kRing - 1 tiles ahead of their use; one barrier per iteration
-// publishes them.
+// publishes them.  Each wave also owns one LDS tile through which its Q rows
+// come in and its O rows go out, as whole 1 KB blocks.
 //
 // The MFMAs are written as inline assembly to fix their register files: the
 // S^T accumulators in VGPRs (the softmax reads them), Q, O^T and l in fixed
