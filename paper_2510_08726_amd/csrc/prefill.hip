@@ -544,8 +544,9 @@ struct Prefill {
 };
 
 // Two waves per SIMD leave each wave 256 registers: the 102 AGPRs named by
-// the inline assembly and at most 152 VGPRs (the compiler does not subtract
-// the inline assembly's AGPRs from its budget by itself).
+// the inline assembly and at most 152 VGPRs.  (By itself the compiler would
+// halve the file once AGPRs are used; the build sets the kernels' AGPR
+// allocation to 104 in the device IR.)
 template <int D, typename T, bool CAUSAL, bool ALIBI>
 __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) void prefill_kernel(PrefillParams p) {
   typedef Prefill<D, T, CAUSAL, ALIBI> PF;
