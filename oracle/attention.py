@@ -34,6 +34,11 @@ design notes):
   hq // (Hq // Hkv) (contiguous groups).
 * ALiBi: bias_ij = -slope[hq] * (i_abs - j) with i_abs = i + (Lk - Lq).  The
   slopes are an input; the oracle takes whatever values the GPU receives.
+* SoftCap (the operator table of the evaluation lists it as attention with a
+  SoftCap score modifier, GQA heads and the causal mask, taken from Gemma 2
+  27B; the paper prints no formula): the scaled product is capped smoothly,
+  ``cap * tanh(p * scale / cap)``, before any bias is added and before the
+  mask.  ``softcap`` is an argument; None or 0 means no cap.
 """
 
 import numpy as np
@@ -53,8 +58,13 @@ def _check(q, k, v, alibi_slopes):
     return B, Hq, Hkv, Lq, Lk, D
 
 
-def scores(q, k, *, scale, causal=False, alibi_slopes=None, b=0, hq=0,
-           rows=None):
+def _softcap(x, cap):
+    """The smooth cap of a scaled score: cap * tanh(x / cap), |result| < cap."""
+    return cap * np.tanh(x / cap)
+
+
+def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, b=0,
+           hq=0, rows=None):
     """Score matrix of one (batch, query head): score_mod(q.k^T) or -inf.
 
     Returns an array [len(rows), Lk] of float64.  ``rows`` selects query rows
@@ -72,6 +82,8 @@ def scores(q, k, *, scale, causal=False, alibi_slopes=None, b=0, hq=0,
     i_abs = i[:, None] + (Lk - Lq)                           # bottom-right aligned row index
     j = np.arange(Lk)[None, :]
     score = p * float(scale)
+    if softcap:
+        score = _softcap(score, float(softcap))
     if alibi_slopes is not None:
         slope = float(np.asarray(alibi_slopes, dtype=np.float64)[hq])
         score = score + (-slope) * (i_abs - j)
@@ -80,11 +92,11 @@ def scores(q, k, *, scale, causal=False, alibi_slopes=None, b=0, hq=0,
     return score
 
 
-def softmax_probs(q, k, *, scale, causal=False, alibi_slopes=None, b=0, hq=0,
-                  rows=None):
+def softmax_probs(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None,
+                  b=0, hq=0, rows=None):
     """Probability matrix P = e / s of one (batch, query head), materialised."""
     score = scores(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes,
-                   b=b, hq=hq, rows=rows)
+                   softcap=softcap, b=b, hq=hq, rows=rows)
     m = score.max(axis=1, keepdims=True)                     # softmax_maxelem
     empty = ~np.isfinite(m)
     m = np.where(empty, 0.0, m)
@@ -93,14 +105,16 @@ def softmax_probs(q, k, *, scale, causal=False, alibi_slopes=None, b=0, hq=0,
     return np.where(empty, 0.0, e / np.where(empty, 1.0, s))
 
 
-def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, rows=None,
-              heads=None):
+def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, softcap=None,
+              rows=None, heads=None):
     """O = softmax(q.k^T * scale + bias, masked) . v, in float64.
 
     q: [B, Hq, Lq, D]; k, v: [B, Hkv, Lk, D]; numpy arrays of any real dtype,
-    converted to float64 exactly one (batch, head) slice at a time.  ``alibi_slopes``: None or [Hq] values.  ``rows``:
-    optional query-row indices to compute (others are skipped, not
-    approximated); ``heads``: optional list of (b, hq) pairs to compute.
+    converted to float64 exactly one (batch, head) slice at a time.
+    ``alibi_slopes``: None or [Hq] values.  ``softcap``: None/0, or the cap > 0
+    of the SoftCap score modifier.  ``rows``: optional query-row indices to
+    compute (others are skipped, not approximated); ``heads``: optional list
+    of (b, hq) pairs to compute.
     Returns float64 [B, Hq, R, D] where R = Lq or len(rows); rows of skipped
     heads are NaN.
     """
@@ -111,7 +125,8 @@ def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, rows=None,
     todo = [(b, h) for b in range(B) for h in range(Hq)] if heads is None else heads
     for b, hq in todo:
         score = scores(q, k, scale=scale, causal=causal,
-                       alibi_slopes=alibi_slopes, b=b, hq=hq, rows=rows)
+                       alibi_slopes=alibi_slopes, softcap=softcap, b=b, hq=hq,
+                       rows=rows)
         m = score.max(axis=1, keepdims=True)                 # softmax_maxelem
         empty = ~np.isfinite(m)                              # row sees no key
         m = np.where(empty, 0.0, m)

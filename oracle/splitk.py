@@ -34,7 +34,8 @@ def chunk_bounds(Lk, num_splits):
     return [(min(s * c, Lk), min((s + 1) * c, Lk)) for s in range(num_splits)]
 
 
-def split_local(q, k, v, *, scale, num_splits, causal=False, alibi_slopes=None):
+def split_local(q, k, v, *, scale, num_splits, causal=False, alibi_slopes=None,
+                softcap=None):
     """Local nests.  Returns (o_l [B,Hq,Lq,S,D], max_l [B,Hq,Lq,S], sum_l [B,Hq,Lq,S])."""
     q = np.asarray(q, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
@@ -49,7 +50,7 @@ def split_local(q, k, v, *, scale, num_splits, causal=False, alibi_slopes=None):
     for b in range(B):
         for hq in range(Hq):
             score = _scores(q, k, scale=scale, causal=causal,
-                            alibi_slopes=alibi_slopes, b=b, hq=hq)
+                            alibi_slopes=alibi_slopes, softcap=softcap, b=b, hq=hq)
             vv = v[b, hq // group]
             for s, (lo, hi) in enumerate(bounds):
                 if hi <= lo:
@@ -81,8 +82,10 @@ def split_global(o_l, max_l, sum_l):
     return np.where(ok[..., None], o_g / np.where(ok, sum_g, 1.0)[..., None], 0.0)
 
 
-def split_k_attention(q, k, v, *, scale, num_splits, causal=False, alibi_slopes=None):
+def split_k_attention(q, k, v, *, scale, num_splits, causal=False, alibi_slopes=None,
+                      softcap=None):
     """Attention by split-k update: local nests then repaired global nests."""
     o_l, max_l, sum_l = split_local(q, k, v, scale=scale, num_splits=num_splits,
-                                    causal=causal, alibi_slopes=alibi_slopes)
+                                    causal=causal, alibi_slopes=alibi_slopes,
+                                    softcap=softcap)
     return split_global(o_l, max_l, sum_l)

@@ -114,3 +114,18 @@ def test_split_local_partials_are_plain_chunk_softmax():
         np.testing.assert_allclose(o_l[0, 0, 0, c] / s_l[0, 0, 0, c],
                                    oracle.attention(q, k[:, :, lo:hi], v[:, :, lo:hi], scale=0.9)[0, 0, 0],
                                    atol=1e-13)
+
+
+@pytest.mark.parametrize("S", [1, 3, 16, 77])
+@pytest.mark.parametrize("alibi", [False, True])
+def test_split_k_with_softcap_equals_plain_definition(S, alibi):
+    """Theorem 2 does not depend on the score modifier: with SoftCap (and GQA)
+    the repaired split-k program still equals the plain definition."""
+    q, k, v = _rand((2, 8, 1, 8), 51) * 3, _rand((2, 2, 77, 8), 52) * 3, _rand((2, 2, 77, 8), 53)
+    sl = alibi_slopes(8).double().numpy() if alibi else None
+    ref = oracle.attention(q, k, v, scale=0.35, causal=True, alibi_slopes=sl, softcap=2.5)
+    o = splitk.split_k_attention(q, k, v, scale=0.35, num_splits=S, causal=True,
+                                 alibi_slopes=sl, softcap=2.5)
+    np.testing.assert_allclose(o, ref, atol=1e-12, rtol=0)
+    plain = oracle.attention(q, k, v, scale=0.35, causal=True, alibi_slopes=sl)
+    assert np.abs(ref - plain).max() > 1e-2          # the cap changes the result at these scores

@@ -130,3 +130,130 @@ def test_mutant_missing_repair_factor_is_caught():
     assert not np.allclose(bad, ref, atol=1e-6)
     good = rolling.rolling_update_attention(q, k, v, scale=0.5, block_n=16)
     np.testing.assert_allclose(good, ref, atol=1e-12)
+
+
+# SoftCap score modifier: cap * tanh(scale * q.k / cap), then the bias, then the mask.
+
+def _softcap_saturated_pin(attn):
+    """|scale q.k| >> cap: every capped score is +-cap exactly, a closed form in e^cap."""
+    cap, Lk = 2.0, 5
+    v = _rand((1, 1, Lk, 3), 41)
+    q = np.zeros((1, 1, 1, 3))
+    q[..., 0] = 1.0
+    k = np.zeros((1, 1, Lk, 3))
+    k[0, 0, :, 0] = -1e3
+    k[0, 0, 0, 0] = 1e3
+    o = attn(q, k, v, scale=1.0, softcap=cap)
+    w = np.array([math.exp(cap)] + [math.exp(-cap)] * (Lk - 1))
+    return np.allclose(o[0, 0, 0], (w[:, None] * v[0, 0]).sum(0) / w.sum(), atol=1e-12)
+
+
+def _softcap_series_pin(attn):
+    """|x| <= 1 << cap: cap tanh(x / cap) = x - x^3/(3 cap^2) + 2 x^5/(15 cap^4) + O(x^7 / cap^6)."""
+    cap, Lk = 4.0, 9
+    x = np.linspace(-1.0, 1.0, Lk)
+    v = _rand((1, 1, Lk, 3), 42)
+    q = np.zeros((1, 1, 1, 3))
+    q[..., 0] = 1.0
+    k = np.zeros((1, 1, Lk, 3))
+    k[0, 0, :, 0] = x
+    o = attn(q, k, v, scale=1.0, softcap=cap)
+    t = x - x ** 3 / (3 * cap ** 2) + 2 * x ** 5 / (15 * cap ** 4)   # remainder < 17 / (315 cap^6) = 1.3e-5
+    w = np.exp(t - t.max())
+    return np.allclose(o[0, 0, 0], (w[:, None] * v[0, 0]).sum(0) / w.sum(), atol=5e-5)
+
+
+def _softcap_huge_cap_pin(attn):
+    """cap -> infinity gives plain attention."""
+    q, k, v = _rand((1, 2, 6, 4), 43), _rand((1, 2, 9, 4), 44), _rand((1, 2, 9, 4), 45)
+    o = attn(q, k, v, scale=0.5, causal=True, softcap=1e8)
+    return np.allclose(o, oracle.attention(q, k, v, scale=0.5, causal=True), atol=1e-9)
+
+
+def _softcap_alibi_pin(attn):
+    """scale 0 caps nothing (tanh 0 = 0), so the ALiBi geometric closed form holds
+    exactly: the bias is added after the cap and the mask comes last."""
+    H, L = 2, 7
+    q, k, v = _rand((1, H, L, 2), 46), _rand((1, H, L, 2), 47), _rand((1, H, L, 2), 48)
+    sl = alibi_slopes(H).double().numpy()
+    o = attn(q, k, v, scale=0.0, causal=True, alibi_slopes=sl, softcap=1.5)
+    for h in range(H):
+        r = math.exp(-sl[h])
+        for i in range(L):
+            w = np.array([r ** (i - j) for j in range(i + 1)])
+            if not np.allclose(o[0, h, i], (w[:, None] * v[0, h, :i + 1]).sum(0) / w.sum(), atol=1e-12):
+                return False
+    return True
+
+
+SOFTCAP_PINS = [_softcap_saturated_pin, _softcap_series_pin, _softcap_huge_cap_pin, _softcap_alibi_pin]
+_ATT = __import__("sys").modules["oracle.attention"]   # the module (oracle.attention is the function)
+
+
+def _patched(name, fn):
+    """The oracle with one of its module functions replaced by a planted mistake."""
+    def mutant(*args, **kw):
+        saved = getattr(_ATT, name)
+        setattr(_ATT, name, fn)
+        try:
+            return oracle.attention(*args, **kw)
+        finally:
+            setattr(_ATT, name, saved)
+    return mutant
+
+
+def test_true_oracle_passes_every_softcap_pin():
+    for pin in SOFTCAP_PINS:
+        assert pin(oracle.attention), pin.__name__
+
+
+def _softcap_caught(mutant):
+    return any(not pin(mutant) for pin in SOFTCAP_PINS)
+
+
+def test_mutant_softcap_ignored_is_caught():
+    assert _softcap_caught(_patched("_softcap", lambda x, cap: x))
+
+
+def test_mutant_softcap_missing_outer_cap_is_caught():
+    assert _softcap_caught(_patched("_softcap", lambda x, cap: np.tanh(x / cap)))
+
+
+def test_mutant_softcap_missing_inner_division_is_caught():
+    assert _softcap_caught(_patched("_softcap", lambda x, cap: cap * np.tanh(x)))
+
+
+def _scores_in_order(bias_inside, mask_first):
+    base = _ATT.scores
+
+    def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, b=0, hq=0, rows=None):
+        if not softcap:
+            return base(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes, b=b, hq=hq, rows=rows)
+        raw = base(q, k, scale=scale, causal=False, alibi_slopes=alibi_slopes if bias_inside else None,
+                   b=b, hq=hq, rows=rows)
+        Lq, Lk = q.shape[2], k.shape[2]
+        i = np.arange(Lq) if rows is None else np.asarray(rows)
+        visible = np.arange(Lk)[None, :] <= i[:, None] + (Lk - Lq)
+        if causal and mask_first:
+            raw = np.where(visible, raw, -np.inf)
+        s = softcap * np.tanh(raw / softcap)
+        if alibi_slopes is not None and not bias_inside:
+            s = s - float(alibi_slopes[hq]) * (i[:, None] + (Lk - Lq) - np.arange(Lk)[None, :])
+        if causal and not mask_first:
+            s = np.where(visible, s, -np.inf)
+        return s
+    return scores
+
+
+def test_mutant_softcap_bias_inside_the_cap_is_caught():
+    assert _softcap_caught(_patched("scores", _scores_in_order(bias_inside=True, mask_first=False)))
+
+
+def test_mutant_softcap_mask_before_the_cap_is_caught():
+    assert _softcap_caught(_patched("scores", _scores_in_order(bias_inside=False, mask_first=True)))
+
+
+def test_softcap_planted_order_helper_matches_oracle_when_correct():
+    """The helper that builds the two order mutants is itself right when given the right order."""
+    good = _patched("scores", _scores_in_order(bias_inside=False, mask_first=False))
+    assert all(pin(good) for pin in SOFTCAP_PINS)
