@@ -13,8 +13,9 @@ D=128, fp16): `value` is its algorithmic TFLOP/s (4*D per visible query/key
 pair).  The decode workloads (B=8, H=32, Lk=8192, D=128; and B=16, Hq=32,
 Hkv=8, Lk=32768, D=128) are reported beside it in `decode` and `decode_gqa` as
 algorithmic GB/s (|Q|+|K|+|V|+|O|), the ALiBi decode workload (the MHA decode
-shape with the ALiBi bias) in `decode_alibi`, and every workload is listed under
-`workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
+shape with the ALiBi bias) in `decode_alibi`, the SoftCap decode workload (B=16,
+Hq=32, Hkv=16, Lk=8192, D=128, cap 50) in `decode_softcap`, and every workload
+is listed under `workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
 bounded sample of the headline workload.
 """
 
@@ -34,6 +35,7 @@ HEADLINE = "causal_mha_prefill"
 DECODE_HEADLINE = "mha_decode"
 DECODE_GQA = "gqa_long_decode"
 DECODE_ALIBI = "alibi_decode"
+DECODE_SOFTCAP = "softcap_decode"
 METRIC = "prefill attn TFLOP/s (% MFMA peak); decode KV-read GB/s (% HBM peak)"
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
@@ -122,7 +124,8 @@ def run_workload(name, steps, warmup):
                          device="cuda")
 
         def fn():
-            pa.attn_decode(q, k, v, o, scale=w.sm_scale, alibi_slopes=sl, num_splits=S, workspace=ws)
+            pa.attn_decode(q, k, v, o, scale=w.sm_scale, alibi_slopes=sl, softcap=w.softcap or None,
+                           num_splits=S, workspace=ws)
         work = decode_bytes(w.B, w.Hq, w.Hkv, w.Lk, w.D)
     else:
         S = None
@@ -133,7 +136,7 @@ def run_workload(name, steps, warmup):
     ms, wall_ms = time_steps(fn, steps, warmup)
     res = {
         "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk, "D": w.D, "dtype": w.dtype,
-        "causal": w.causal, "alibi": w.alibi, "ms_per_step": round(ms, 5),
+        "causal": w.causal, "alibi": w.alibi, "softcap": w.softcap, "ms_per_step": round(ms, 5),
         "host_wall_ms_per_step": round(wall_ms, 5),
     }
     if w.decode:
@@ -232,6 +235,7 @@ def main():
     decode = decode_entry(DECODE_HEADLINE, results[DECODE_HEADLINE])
     decode_gqa = decode_entry(DECODE_GQA, results[DECODE_GQA])
     decode_alibi = decode_entry(DECODE_ALIBI, results[DECODE_ALIBI])
+    decode_softcap = decode_entry(DECODE_SOFTCAP, results[DECODE_SOFTCAP])
     line = {
         "metric": METRIC, "value": head["TFLOP/s"], "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
@@ -243,6 +247,7 @@ def main():
         "decode": decode,
         "decode_gqa": decode_gqa,
         "decode_alibi": decode_alibi,
+        "decode_softcap": decode_softcap,
         "workloads": results,
     }
     if not args.no_cpu_baseline:

@@ -64,7 +64,8 @@ typedef enum {
 typedef enum {
   ATTN_OK = 0,
   ATTN_ERR_NULL = -1,        /* a required pointer is NULL */
-  ATTN_ERR_SHAPE = -2,       /* a size is < 1, Hq % Hkv != 0, num_splits < 0, or a size overflows */
+  ATTN_ERR_SHAPE = -2,       /* a size is < 1, Hq % Hkv != 0, num_splits < 0, a size overflows,
+                                scale is not finite, or softcap is negative or not finite */
   ATTN_ERR_UNSUPPORTED = -3, /* head dim not 64 or 128, or unknown dtype */
   ATTN_ERR_WORKSPACE = -4,   /* decode workspace smaller than attn_decode_workspace_bytes() */
   ATTN_ERR_HIP = -5          /* a HIP launch failed; see attn_last_hip_error() */
@@ -119,6 +120,11 @@ int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D);
  *   Q [B, Hq, 1, D], K and V [B, Hkv, Lk, D], O [B, Hq, 1, D]   (device)
  *   The query is the token at position Lk - 1, so every key is visible (the
  *   causal mask is a no-op).  alibi_slopes as for attn_fwd, with i = Lk - 1.
+ *   softcap     0 for none, or cap > 0: the SoftCap operator of the paper's
+ *               evaluation (its operator table: attention with a SoftCap
+ *               score modifier, GQA heads and the causal mask, from Gemma 2;
+ *               the formula is not printed).  Each scaled score becomes
+ *               cap * tanh(score * scale / cap) before the ALiBi bias is added.
  *   num_splits  >= 1 chunks of ceil(Lk / num_splits) keys (the last chunk may
  *               be short, chunks past Lk are empty), or 0 for the heuristic.
  *   workspace   device buffer of at least attn_decode_workspace_bytes(B, Hq,
@@ -131,7 +137,7 @@ int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D);
  */
 int attn_decode(const void* Q, const void* K, const void* V, void* O,
                 int B, int Hq, int Hkv, int Lk, int D,
-                float scale, const float* alibi_slopes, int num_splits,
+                float scale, const float* alibi_slopes, float softcap, int num_splits,
                 void* workspace, size_t workspace_bytes,
                 attn_dtype dtype, hipStream_t stream);
 

@@ -62,7 +62,7 @@ def load_library():
     vp, ci, cf, cs = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, vp, ci, vp]
     lib.attn_fwd.restype = ci
-    lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, ci, vp, cs, ci, vp]
+    lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, cf, ci, vp, cs, ci, vp]
     lib.attn_decode.restype = ci
     lib.attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci]
     lib.attn_decode_workspace_bytes.restype = cs
@@ -151,11 +151,12 @@ def attn_decode_num_splits(B, Hq, Hkv, Lk, D):
     return load_library().attn_decode_num_splits(B, Hq, Hkv, Lk, D)
 
 
-def attn_decode(q, k, v, o=None, *, scale=None, alibi_slopes=None, num_splits=0,
+def attn_decode(q, k, v, o=None, *, scale=None, alibi_slopes=None, softcap=None, num_splits=0,
                 workspace=None, stream=None):
     """Single-token decode by split-k: q [B, Hq, 1, D] against k, v [B, Hkv, Lk, D].
 
-    ``num_splits`` = 0 lets the library choose.  ``workspace`` (uint8 GPU
+    ``softcap``: None, or the cap > 0 of the SoftCap score modifier
+    (cap * tanh(scale q.k / cap)).  ``num_splits`` = 0 lets the library choose.  ``workspace`` (uint8 GPU
     tensor) is allocated when not given.  Returns ``o`` [B, Hq, 1, D].
     """
     _check_tensors(q, k, v, alibi_slopes)
@@ -174,7 +175,7 @@ def attn_decode(q, k, v, o=None, *, scale=None, alibi_slopes=None, num_splits=0,
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
     _check(lib.attn_decode(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lk, D, sc,
-                           _ptr(alibi_slopes), int(num_splits), _ptr(workspace),
+                           _ptr(alibi_slopes), float(softcap or 0.0), int(num_splits), _ptr(workspace),
                            workspace.numel() * workspace.element_size(), _DTYPE_CODE[q.dtype],
                            _stream(stream)))
     return o

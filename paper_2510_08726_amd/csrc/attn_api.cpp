@@ -139,11 +139,12 @@ size_t attn_decode_workspace_bytes(int B, int Hq, int D, int num_splits) {
 
 int attn_decode(const void* Q, const void* K, const void* V, void* O,
                 int B, int Hq, int Hkv, int Lk, int D,
-                float scale, const float* alibi_slopes, int num_splits,
+                float scale, const float* alibi_slopes, float softcap, int num_splits,
                 void* workspace, size_t workspace_bytes,
                 attn_dtype dtype, hipStream_t stream) {
   if (!Q || !K || !V || !O || !workspace) return ATTN_ERR_NULL;
   if (!shape_ok(B, Hq, Hkv, 1, Lk) || num_splits < 0 || !std::isfinite(scale)) return ATTN_ERR_SHAPE;
+  if (!std::isfinite(softcap) || softcap < 0.f) return ATTN_ERR_SHAPE;
   if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
   if (!sizes_fit(B, Hq, Hkv, 1, Lk, D)) return ATTN_ERR_SHAPE;
   const int S = num_splits ? num_splits : attn_decode_num_splits(B, Hq, Hkv, Lk, D);
@@ -166,6 +167,8 @@ int attn_decode(const void* Q, const void* K, const void* V, void* O,
   p.chunk = (Lk + S - 1) / S;
   p.bf16 = dtype == ATTN_BF16;
   p.c = scale * kLog2e;
+  p.cap_k2 = softcap > 0.f ? 2.f / softcap : 0.f;
+  p.cap_cl = softcap > 0.f ? softcap * kLog2e : 0.f;
   hipError_t e = attn::launch_decode(p, stream);
   return e == hipSuccess ? ATTN_OK : hip_fail(e);
 }

@@ -38,6 +38,15 @@ __device__ __forceinline__ float dpp_move(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
 }
 
+// SoftCap of a score in log2 units (x = s log2 e): cap tanh(s / cap) log2 e,
+// from tanh(y) = 1 - 2 / (1 + e^{2y}) with e^{2y} = 2^(x k2); k2 = 2 / cap,
+// cl = cap log2 e.  The exponential saturates to inf or 0 for large |x|, which
+// gives +-cl exactly.
+__device__ __forceinline__ float soft_cap(float x, float k2, float cl) {
+  const float e = fast_exp2(x * k2);
+  return __builtin_fmaf(-2.f * cl, __builtin_amdgcn_rcpf(1.f + e), cl);
+}
+
 template <int LPK>
 __device__ __forceinline__ float group_sum(float x) {
   x += dpp_move<0xB1>(x);   // quad_perm [1,0,3,2]
@@ -47,7 +56,7 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
-template <int D, typename T, int GH, bool ALIBI>
+template <int D, typename T, int GH, bool ALIBI, bool CAP>
 __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) {
   typedef Elem<T> E;
   constexpr int LPK = D / 8;               // lanes per key row
@@ -124,6 +133,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
         part = E::dot2(qv[g].z, kr[u].z, part);
         part = E::dot2(qv[g].w, kr[u].w, part);
         float x = group_sum<LPK>(part) * c;
+        if (CAP) x = soft_cap(x, p.cap_k2, p.cap_cl);
         if (ALIBI) x = __builtin_fmaf(sl2[g], (float)(key[u] - (Lk - 1)), x);
         sc[u] = key[u] < ke ? x : kNegInf;
         mt = fmaxf(mt, sc[u]);
@@ -225,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
 // (the compute definition casts exp to the input type before the second
 // matmul), while the chunk's exp-sum l is accumulated from the fp32 values,
 // as that definition sums them.
-template <int D, typename T, bool ALIBI>
+template <int D, typename T, bool ALIBI, bool CAP>
 __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
   typedef Elem<T> E;
   typedef typename E::vec8 vec8;
@@ -355,6 +365,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
     for (int r = 0; r < 16; ++r) {
       const int key = k0 + 8 * (r / 4) + 4 * hh + (r % 4);
       float v = sacc[r] * c;
+      if (CAP) v = soft_cap(v, p.cap_k2, p.cap_cl);
       if (ALIBI) v = __builtin_fmaf(sl2, (float)(key - (Lk - 1)), v);
       x[r] = key < kw1 ? v : kNegInf;
       tmax = fmaxf(tmax, x[r]);
@@ -504,10 +515,15 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams p) {
 template <int D, typename T, int GH>
 hipError_t launch_split(const DecodeParams& p, hipStream_t stream) {
   const int nblocks = p.splits * (p.group / GH) * p.Hkv * p.B;
-  if (p.slopes)
-    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, true>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  const dim3 grid(nblocks), block(kThreads);
+  if (p.slopes && p.cap_cl != 0.f)
+    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, true, true>), grid, block, 0, stream, p);
+  else if (p.slopes)
+    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, true, false>), grid, block, 0, stream, p);
+  else if (p.cap_cl != 0.f)
+    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, false, true>), grid, block, 0, stream, p);
   else
-    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, false>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((decode_split_kernel<D, T, GH, false, false>), grid, block, 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((decode_combine_kernel<D, T>), dim3(p.B * p.Hq), dim3(D), 0, stream, p);
@@ -517,10 +533,15 @@ hipError_t launch_split(const DecodeParams& p, hipStream_t stream) {
 template <int D, typename T>
 hipError_t launch_mfma(const DecodeParams& p, hipStream_t stream) {
   const int nblocks = p.splits * p.Hkv * p.B;
-  if (p.slopes)
-    hipLaunchKernelGGL((decode_mfma_kernel<D, T, true>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  const dim3 grid(nblocks), block(kThreads);
+  if (p.slopes && p.cap_cl != 0.f)
+    hipLaunchKernelGGL((decode_mfma_kernel<D, T, true, true>), grid, block, 0, stream, p);
+  else if (p.slopes)
+    hipLaunchKernelGGL((decode_mfma_kernel<D, T, true, false>), grid, block, 0, stream, p);
+  else if (p.cap_cl != 0.f)
+    hipLaunchKernelGGL((decode_mfma_kernel<D, T, false, true>), grid, block, 0, stream, p);
   else
-    hipLaunchKernelGGL((decode_mfma_kernel<D, T, false>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((decode_mfma_kernel<D, T, false, false>), grid, block, 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((decode_combine_kernel<D, T>), dim3(p.B * p.Hq), dim3(D), 0, stream, p);

@@ -40,6 +40,8 @@ struct DecodeParams {
   int chunk;            // ceil(Lk / S)
   int bf16;
   float c;              // scale * log2(e)
+  float cap_k2;         // SoftCap: 2 / cap
+  float cap_cl;         // SoftCap: cap * log2(e), or 0 for no cap
 };
 
 int prefill_block_rows();

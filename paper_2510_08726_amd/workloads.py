@@ -35,6 +35,7 @@ class Workload:
     seed: int = 0
     num_splits: int = 0
     scale: float = field(default=None)
+    softcap: float = 0.0      # SoftCap cap (0: none)
 
     @property
     def sm_scale(self):
@@ -42,8 +43,10 @@ class Workload:
 
 
 # The six shapes the headline metric is quoted on, then ALiBi decode (the MHA
-# decode shape with the ALiBi bias).  Prefill: Lq == Lk.  Decode: one query
-# token (Lq = 1) against a KV cache of Lk keys.
+# decode shape with the ALiBi bias) and SoftCap decode (Gemma 2 27B's
+# attention: 32 query heads on 16 KV heads of dim 128, logits capped at 50).
+# Prefill: Lq == Lk.  Decode: one query token (Lq = 1) against a KV cache of
+# Lk keys.
 WORKLOADS = {
     "tiny_noncausal": Workload("tiny_noncausal", 1, 2, 2, 128, 128, 64, "f16",
                                seed=1),
@@ -60,6 +63,8 @@ WORKLOADS = {
                                 "f16", decode=True, seed=6),
     "alibi_decode": Workload("alibi_decode", 8, 32, 32, 1, 8192, 128, "f16",
                              alibi=True, decode=True, seed=7),
+    "softcap_decode": Workload("softcap_decode", 16, 32, 16, 1, 8192, 128, "f16",
+                               decode=True, seed=8, softcap=50.0),
 }
 
 

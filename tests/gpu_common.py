@@ -50,7 +50,7 @@ def run_fwd(q, k, v, *, scale, causal=False, slopes=None):
     return o
 
 
-def oracle_fwd(q, k, v, *, scale, causal=False, slopes=None, rows=None, heads=None):
+def oracle_fwd(q, k, v, *, scale, causal=False, slopes=None, softcap=None, rows=None, heads=None):
     sl = None if slopes is None else host64(slopes)
     return oracle.attention(host32(q), host32(k), host32(v), scale=scale, causal=causal,
-                            alibi_slopes=sl, rows=rows, heads=heads)
+                            alibi_slopes=sl, softcap=softcap, rows=rows, heads=heads)

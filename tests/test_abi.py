@@ -69,8 +69,8 @@ def test_fwd_rejects_bad_arguments(lib, kw, code):
 
 
 def dec(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=2, Hq=8, Hkv=2, Lk=100, D=128, scale=0.1,
-        slopes=NULL, S=4, ws=FAKE, ws_bytes=1 << 30, dtype=0):
-    return lib.attn_decode(q, k, v, o, B, Hq, Hkv, Lk, D, scale, slopes, S, ws, ws_bytes, dtype, NULL)
+        slopes=NULL, cap=0.0, S=4, ws=FAKE, ws_bytes=1 << 30, dtype=0):
+    return lib.attn_decode(q, k, v, o, B, Hq, Hkv, Lk, D, scale, slopes, cap, S, ws, ws_bytes, dtype, NULL)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -78,6 +78,8 @@ def dec(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=2, Hq=8, Hkv=2, Lk=100, D=128, sc
     (dict(B=0), pa.ATTN_ERR_SHAPE), (dict(Hq=6, Hkv=4), pa.ATTN_ERR_SHAPE),
     (dict(Lk=0), pa.ATTN_ERR_SHAPE), (dict(S=-1), pa.ATTN_ERR_SHAPE),
     (dict(scale=float("nan")), pa.ATTN_ERR_SHAPE),
+    (dict(cap=-1.0), pa.ATTN_ERR_SHAPE), (dict(cap=float("nan")), pa.ATTN_ERR_SHAPE),
+    (dict(cap=float("inf")), pa.ATTN_ERR_SHAPE),
     (dict(D=32), pa.ATTN_ERR_UNSUPPORTED), (dict(dtype=7), pa.ATTN_ERR_UNSUPPORTED),
     (dict(ws_bytes=100), pa.ATTN_ERR_WORKSPACE),
     (dict(ws=ctypes.c_void_p(0x1004)), pa.ATTN_ERR_WORKSPACE),   # not 16-byte aligned

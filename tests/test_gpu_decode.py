@@ -20,7 +20,7 @@ from gpu_common import assert_close, host32, host64, oracle_fwd, run_fwd
 pytestmark = pytest.mark.gpu
 
 
-def run_decode(q, k, v, *, scale, slopes=None, num_splits=0):
+def run_decode(q, k, v, *, scale, slopes=None, softcap=None, num_splits=0):
     dev = torch.device("cuda")
     B, Hq, _, D = q.shape
     Hkv, Lk = k.shape[1], k.shape[2]
@@ -28,7 +28,7 @@ def run_decode(q, k, v, *, scale, slopes=None, num_splits=0):
     ws = torch.empty(pa.attn_decode_workspace_bytes(B, Hq, D, S), dtype=torch.uint8, device=dev)
     o = pa.attn_decode(q.to(dev), k.to(dev), v.to(dev), scale=scale,
                        alibi_slopes=None if slopes is None else slopes.to(dev),
-                       num_splits=num_splits, workspace=ws)
+                       softcap=softcap, num_splits=num_splits, workspace=ws)
     torch.cuda.synchronize()
     return o, ws, S
 
@@ -104,14 +104,73 @@ def test_decode_is_deterministic():
 def _workload_run(name):
     w = WORKLOADS[name]
     q, k, v, sl = make_inputs(w)
-    o, ws, S = run_decode(q, k, v, scale=w.sm_scale, slopes=sl, num_splits=w.num_splits)
+    o, ws, S = run_decode(q, k, v, scale=w.sm_scale, slopes=sl, softcap=w.softcap or None,
+                          num_splits=w.num_splits)
     return w, q, k, v, sl, o.cpu()
 
 
-@pytest.mark.parametrize("name", ["mha_decode", "gqa_long_decode", "alibi_decode"])
+@pytest.mark.parametrize("name", ["mha_decode", "gqa_long_decode", "alibi_decode", "softcap_decode"])
 def test_decode_workload_full(name):
     """Every output row of the full-size decode workloads vs the oracle."""
     print(f"decode workload {name}", flush=True)
     w, q, k, v, sl, o = _workload_run(name)
-    ref = oracle_fwd(q, k, v, scale=w.sm_scale, causal=True, slopes=sl)
+    ref = oracle_fwd(q, k, v, scale=w.sm_scale, causal=True, slopes=sl, softcap=w.softcap or None)
     assert_close(host32(o), ref, name)
+
+
+SOFTCAP_CASES = [  # B, Hq, Hkv, Lk, D, dtype, S, alibi, cap, score gain
+    (2, 8, 8, 1000, 128, "f16", 3, False, 2.0, 4.0),     # one head per KV head: vector kernel
+    (2, 8, 2, 777, 64, "bf16", 5, False, 1.0, 4.0),      # 4 query heads per KV head: matrix kernel
+    (1, 32, 16, 2500, 128, "f16", 0, False, 5.0, 8.0),   # Gemma 2 27B head layout
+    (1, 16, 1, 300, 128, "bf16", 4, True, 3.0, 4.0),     # 16 per KV head, with ALiBi after the cap
+    (2, 6, 6, 333, 64, "f16", 2, True, 0.5, 1.0),        # vector kernel with ALiBi after the cap
+    (1, 4, 2, 1, 128, "f16", 3, False, 1.0, 4.0),        # one key, two empty chunks
+]
+
+
+@pytest.mark.parametrize("case", SOFTCAP_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_decode_softcap_matches_oracle(case):
+    """SoftCap decode vs the oracle.  The query is scaled up ("score gain") so
+    that the scores reach the cap and the capped result differs from the
+    uncapped one by far more than the tolerance."""
+    B, Hq, Hkv, Lk, D, dt, S, alibi, cap, gain = case
+    print(f"softcap decode case {case}", flush=True)
+    q, k, v = random_tensors([(B, Hq, 1, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], dt,
+                             seed=zlib.crc32(repr(case).encode()) % 1000)
+    q = (q.float() * gain).to(q.dtype)
+    sl = alibi_slopes(Hq) if alibi else None
+    scale = D ** -0.5
+    o, ws, Sres = run_decode(q, k, v, scale=scale, slopes=sl, softcap=cap, num_splits=S)
+    ref = oracle_fwd(q, k, v, scale=scale, causal=True, slopes=sl, softcap=cap)
+    assert_close(host32(o), ref, f"softcap decode {case}")
+    if Lk > 1:
+        plain = oracle_fwd(q, k, v, scale=scale, causal=True, slopes=sl)
+        assert np.abs(plain - ref).max() > 0.05, "the cap must matter in this case"
+    # the local nests carry the capped scores
+    o_l, m_l, s_l = [t.cpu().numpy().astype(np.float64) for t in pa.decode_partials(ws, B, Hq, D, Sres)]
+    ro, rm, rs = splitk.split_local(host32(q), host32(k), host32(v), scale=scale, num_splits=Sres,
+                                    causal=True, alibi_slopes=None if sl is None else host64(sl),
+                                    softcap=cap)
+    live = ~np.isneginf(rm[:, :, 0])
+    assert np.array_equal(np.isneginf(m_l), ~live)
+    np.testing.assert_allclose(m_l[live], rm[:, :, 0][live], atol=1e-4, rtol=1e-5)
+    np.testing.assert_allclose(s_l[live], rs[:, :, 0][live], rtol=2e-4)
+
+
+def test_decode_softcap_saturates_exactly():
+    """Scores far beyond the cap: every capped score is +-cap, so the output is
+    the closed-form mix e^cap V_j* + e^-cap (others), whatever the kernel."""
+    B, Hq, Hkv, Lk, D, cap = 1, 2, 2, 64, 64, 1.5
+    q = torch.zeros(B, Hq, 1, D)
+    q[..., 0] = 1.0
+    k = torch.zeros(B, Hkv, Lk, D)
+    k[..., 0] = -1000.0
+    k[:, :, 17, 0] = 1000.0
+    v = random_tensors([(B, Hkv, Lk, D)], "f16", seed=77)[0]
+    q, k = q.half(), k.half()
+    o = host32(run_decode(q, k, v, scale=1.0, softcap=cap, num_splits=4)[0])
+    w = np.full(Lk, np.exp(-cap))
+    w[17] = np.exp(cap)
+    ref = (w[:, None] * host64(v)[0]).sum(1) / w.sum()          # [Hq, D]
+    assert np.all(np.isfinite(o))
+    np.testing.assert_allclose(o[0, :, 0], ref, atol=2e-3)
