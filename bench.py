@@ -14,8 +14,9 @@ pair).  The decode workloads (B=8, H=32, Lk=8192, D=128; and B=16, Hq=32,
 Hkv=8, Lk=32768, D=128) are reported beside it in `decode` and `decode_gqa` as
 algorithmic GB/s (|Q|+|K|+|V|+|O|), the ALiBi decode workload (the MHA decode
 shape with the ALiBi bias) in `decode_alibi`, the SoftCap decode workload (B=16,
-Hq=32, Hkv=16, Lk=8192, D=128, cap 50) in `decode_softcap`, and every workload
-is listed under `workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
+Hq=32, Hkv=16, Lk=8192, D=128, cap 50) in `decode_softcap`, the SoftCap causal
+prefill (B=2, Hq=32, Hkv=16, L=4096, D=128, cap 50) in `prefill_softcap`, and
+every workload is listed under `workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
 bounded sample of the headline workload.
 """
 
@@ -36,6 +37,7 @@ DECODE_HEADLINE = "mha_decode"
 DECODE_GQA = "gqa_long_decode"
 DECODE_ALIBI = "alibi_decode"
 DECODE_SOFTCAP = "softcap_decode"
+PREFILL_SOFTCAP = "softcap_causal_prefill"
 METRIC = "prefill attn TFLOP/s (% MFMA peak); decode KV-read GB/s (% HBM peak)"
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
@@ -131,7 +133,8 @@ def run_workload(name, steps, warmup):
         S = None
 
         def fn():
-            pa.attn_fwd(q, k, v, o, causal=w.causal, scale=w.sm_scale, alibi_slopes=sl)
+            pa.attn_fwd(q, k, v, o, causal=w.causal, scale=w.sm_scale, alibi_slopes=sl,
+                        softcap=w.softcap or None)
         work = prefill_flops(w.B, w.Hq, w.Lq, w.Lk, w.D, w.causal)
     ms, wall_ms = time_steps(fn, steps, warmup)
     res = {
@@ -236,6 +239,14 @@ def main():
     decode_gqa = decode_entry(DECODE_GQA, results[DECODE_GQA])
     decode_alibi = decode_entry(DECODE_ALIBI, results[DECODE_ALIBI])
     decode_softcap = decode_entry(DECODE_SOFTCAP, results[DECODE_SOFTCAP])
+    ps = results[PREFILL_SOFTCAP]
+    prefill_softcap = {
+        "workload": PREFILL_SOFTCAP, "value": ps["TFLOP/s"], "unit": "TFLOP/s", "ms_per_step": ps["ms_per_step"],
+        "roofline": {"bound": "mfma", "achieved": ps["TFLOP/s"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(ps["TFLOP/s"] / MFMA_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic("prefill", PREFILL_SOFTCAP),
+                     "per_launch": f"{ps['flops_per_step']} algorithmic flops (4*D per visible query/key pair)"},
+    }
     line = {
         "metric": METRIC, "value": head["TFLOP/s"], "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
@@ -248,6 +259,7 @@ def main():
         "decode_gqa": decode_gqa,
         "decode_alibi": decode_alibi,
         "decode_softcap": decode_softcap,
+        "prefill_softcap": prefill_softcap,
         "workloads": results,
     }
     if not args.no_cpu_baseline:

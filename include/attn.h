@@ -66,7 +66,8 @@ typedef enum {
   ATTN_ERR_NULL = -1,        /* a required pointer is NULL */
   ATTN_ERR_SHAPE = -2,       /* a size is < 1, Hq % Hkv != 0, num_splits < 0, a size overflows,
                                 scale is not finite, or softcap is negative or not finite */
-  ATTN_ERR_UNSUPPORTED = -3, /* head dim not 64 or 128, or unknown dtype */
+  ATTN_ERR_UNSUPPORTED = -3, /* head dim not 64 or 128, unknown dtype, or (attn_fwd) softcap
+                                without the causal mask or together with ALiBi */
   ATTN_ERR_WORKSPACE = -4,   /* decode workspace smaller than attn_decode_workspace_bytes() */
   ATTN_ERR_HIP = -5          /* a HIP launch failed; see attn_last_hip_error() */
 } attn_status;
@@ -79,13 +80,17 @@ typedef enum {
  *   causal  0 or 1 (non-zero means 1)
  *   scale   finite float
  *   alibi_slopes  device float[Hq] or NULL
+ *   softcap 0 for none, or cap > 0 (causal and without ALiBi only): each
+ *           scaled score becomes cap * tanh(score * scale / cap) before the
+ *           mask, as described for attn_decode
  *
- * Errors: ATTN_ERR_NULL if Q, K, V or O is NULL; ATTN_ERR_SHAPE for bad sizes;
- * ATTN_ERR_UNSUPPORTED for D or dtype; ATTN_ERR_HIP if the launch fails.
+ * Errors: ATTN_ERR_NULL if Q, K, V or O is NULL; ATTN_ERR_SHAPE for bad sizes
+ * or a negative / non-finite softcap; ATTN_ERR_UNSUPPORTED for D, dtype, or
+ * softcap without causal or with ALiBi; ATTN_ERR_HIP if the launch fails.
  */
 int attn_fwd(const void* Q, const void* K, const void* V, void* O,
              int B, int Hq, int Hkv, int Lq, int Lk, int D,
-             int causal, float scale, const float* alibi_slopes,
+             int causal, float scale, const float* alibi_slopes, float softcap,
              attn_dtype dtype, hipStream_t stream);
 
 /*

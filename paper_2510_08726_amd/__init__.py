@@ -60,7 +60,7 @@ def load_library():
             "or `python paper_2510_08726_amd/build.py` first")
     lib = ctypes.CDLL(path)
     vp, ci, cf, cs = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
-    lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, vp, ci, vp]
+    lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, vp, cf, ci, vp]
     lib.attn_fwd.restype = ci
     lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, cf, ci, vp, cs, ci, vp]
     lib.attn_decode.restype = ci
@@ -120,12 +120,14 @@ def _check_tensors(q, k, v, slopes):
         _require(slopes.numel() == q.shape[1], "alibi_slopes needs one value per query head")
 
 
-def attn_fwd(q, k, v, o=None, *, causal=False, scale=None, alibi_slopes=None, stream=None):
+def attn_fwd(q, k, v, o=None, *, causal=False, scale=None, alibi_slopes=None, softcap=None,
+             stream=None):
     """O = softmax(Q K^T * scale + bias) V by the fused prefill kernel.
 
     q [B, Hq, Lq, D], k and v [B, Hkv, Lk, D] (float16 or bfloat16, contiguous,
     on the GPU); ``o`` is written if given, else allocated.  ``scale``
-    defaults to 1/sqrt(D).  Returns ``o``.
+    defaults to 1/sqrt(D).  ``softcap``: None, or the cap > 0 of the SoftCap
+    score modifier (causal, without ALiBi).  Returns ``o``.
     """
     _check_tensors(q, k, v, alibi_slopes)
     B, Hq, Lq, D = q.shape
@@ -138,7 +140,8 @@ def attn_fwd(q, k, v, o=None, *, causal=False, scale=None, alibi_slopes=None, st
     sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
     lib = load_library()
     _check(lib.attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lq, Lk, D,
-                        int(bool(causal)), sc, _ptr(alibi_slopes), _DTYPE_CODE[q.dtype],
+                        int(bool(causal)), sc, _ptr(alibi_slopes), float(softcap or 0.0),
+                        _DTYPE_CODE[q.dtype],
                         _stream(stream)))
     return o
 

@@ -77,11 +77,13 @@ int attn_last_hip_error(void) { return g_last_hip_error; }
 
 int attn_fwd(const void* Q, const void* K, const void* V, void* O,
              int B, int Hq, int Hkv, int Lq, int Lk, int D,
-             int causal, float scale, const float* alibi_slopes,
+             int causal, float scale, const float* alibi_slopes, float softcap,
              attn_dtype dtype, hipStream_t stream) {
   if (!Q || !K || !V || !O) return ATTN_ERR_NULL;
   if (!shape_ok(B, Hq, Hkv, Lq, Lk) || !std::isfinite(scale)) return ATTN_ERR_SHAPE;
+  if (!std::isfinite(softcap) || softcap < 0.f) return ATTN_ERR_SHAPE;
   if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
+  if (softcap > 0.f && (!causal || alibi_slopes)) return ATTN_ERR_UNSUPPORTED;
   if (!sizes_fit(B, Hq, Hkv, Lq, Lk, D)) return ATTN_ERR_SHAPE;
   const int bm = attn::prefill_block_rows();
   const int64_t nqb = ((int64_t)Lq + bm - 1) / bm;
@@ -94,7 +96,9 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
   p.group = Hq / Hkv;
   p.causal = causal ? 1 : 0;
   p.bf16 = dtype == ATTN_BF16;
-  if (alibi_slopes) {
+  p.cap_k2 = softcap > 0.f ? 2.f / softcap : 0.f;
+  p.cap_cl = softcap > 0.f ? softcap * kLog2e : 0.f;
+  if (alibi_slopes || softcap > 0.f) {
     p.c = scale * kLog2e;
     p.qsign = 0;
   } else {

@@ -38,15 +38,6 @@ __device__ __forceinline__ float dpp_move(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
 }
 
-// SoftCap of a score in log2 units (x = s log2 e): cap tanh(s / cap) log2 e,
-// from tanh(y) = 1 - 2 / (1 + e^{2y}) with e^{2y} = 2^(x k2); k2 = 2 / cap,
-// cl = cap log2 e.  The exponential saturates to inf or 0 for large |x|, which
-// gives +-cl exactly.
-__device__ __forceinline__ float soft_cap(float x, float k2, float cl) {
-  const float e = fast_exp2(x * k2);
-  return __builtin_fmaf(-2.f * cl, __builtin_amdgcn_rcpf(1.f + e), cl);
-}
-
 template <int LPK>
 __device__ __forceinline__ float group_sum(float x) {
   x += dpp_move<0xB1>(x);   // quad_perm [1,0,3,2]

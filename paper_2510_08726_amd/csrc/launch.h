@@ -16,8 +16,10 @@ struct PrefillParams {
   int group;            // Hq / Hkv
   int causal;
   int bf16;
-  float c;              // |scale| * log2(e) without ALiBi, scale * log2(e) with it
-  unsigned qsign;       // 0x80008000 to negate Q (negative scale without ALiBi), else 0
+  float c;              // |scale| * log2(e) without ALiBi or SoftCap, scale * log2(e) with either
+  unsigned qsign;       // 0x80008000 to negate Q (negative scale, no ALiBi or SoftCap), else 0
+  float cap_k2;         // SoftCap: 2 / cap
+  float cap_cl;         // SoftCap: cap * log2(e), or 0 for no cap
   int nqb;              // query blocks per head
   int nheads;           // B * Hq, set by the launcher
   int nitems;           // nqb * nheads, set by the launcher

@@ -225,7 +225,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 //   exp    8 steps: 2 exponentials and their packing
 //   max    4 steps: 4 scores folded into this lane's partial max
 // (the exp-sum is accumulated by rowsum MFMAs beside P.V).
-template <bool PREP, bool MASKED, bool ALIBI>
+template <bool PREP, bool MASKED, bool ALIBI, bool CAP>
 struct SoftPlan {
   // Steps [0, MAX0) prepare the scores, four registers a step; then come 8
   // exponential steps (two registers each) and 4 steps of the lane's running
@@ -236,7 +236,7 @@ struct SoftPlan {
   static constexpr int exp_index(int k) { return 2 * ((k - MAX0) / 3) + (k - MAX0) % 3; }
   static constexpr int max_index(int k) { return (k - MAX0) / 3; }
   static constexpr int weight(int k) {
-    if (k < MAX0) return (ALIBI ? 8 : 0) + (MASKED ? 8 : 0);
+    if (k < MAX0) return (ALIBI ? 8 : 0) + (MASKED ? 8 : 0) + (CAP ? 52 : 0);
     return is_exp(k) ? 26 : 10;
   }
   // First step of slot s when the steps are spread over ns slots.
@@ -252,8 +252,11 @@ struct SoftPlan {
   }
 };
 
-template <int D, typename T, bool CAUSAL, bool ALIBI>
+template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP>
 struct Prefill {
+  // Scores are prepared in log2 units (the scale folded in) whenever a bias
+  // or the cap has to act on the scaled value.
+  static constexpr bool LOG2 = ALIBI || CAP;
   typedef Elem<T> E;
   typedef Mma<T> M;
   typedef typename E::vec8 vec8;
@@ -272,7 +275,7 @@ struct Prefill {
   // the V ring is shallower too.  Deeper K rings measured slower: the
   // registers they hold push the per-item code into scratch.
   static constexpr int PFD_K = 1;
-  static constexpr int PFD_V = ALIBI ? 1 : 3;
+  static constexpr int PFD_V = LOG2 ? 1 : 3;
   template <bool IS_K> static constexpr int pfd() { return IS_K ? PFD_K : PFD_V; }
   static_assert(NG % (PFD_K + 1) == 0 && NG % (PFD_V + 1) == 0, "fragment ring positions must repeat every iteration");
   static_assert(kOAgpr + 16 * DB <= kQAgpr && kQAgpr + 4 * KX <= kLAgpr, "AGPR map");
@@ -297,7 +300,8 @@ struct Prefill {
     int v[DB][2];
   };
   struct TileArgs {
-    float c;      // scale * log2(e) (with ALiBi) or max(|scale| * log2(e), tiny)
+    float c;      // scale * log2(e) (with ALiBi or SoftCap) or max(|scale| * log2(e), tiny)
+    float k2, cl; // SoftCap: 2 / cap and cap * log2(e)
     float sl2;    // ALiBi slope * log2(e)
     float abase;  // ALiBi bias of key j0 + 4 hh relative to the wave's first row
     int lim;      // last visible key offset (key - j0 - 4 hh) of this lane's row
@@ -379,8 +383,8 @@ struct Prefill {
   // row to -inf before the max.
   template <int K, bool PREP, bool MASKED>
   static __device__ __forceinline__ void soft_step(State& st, Scores& sc, Probs& pr, TileArgs& ta) {
-    typedef SoftPlan<PREP, MASKED, ALIBI> P;
-    const float ce = ALIBI ? 1.f : ta.c;
+    typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
+    const float ce = LOG2 ? 1.f : ta.c;
     if constexpr (K < P::MAX0) {
       constexpr int r0 = 4 * K;
       // Registers r0 .. r0 + 3 hold keys kconst(r0) + 0..3: their biases are
@@ -394,7 +398,12 @@ struct Prefill {
       }
 #pragma unroll
       for (int r = r0; r < r0 + 4; ++r) {
-        if constexpr (ALIBI) sc[r] = __builtin_fmaf(sc[r], ta.c, b[r - r0]);
+        if constexpr (CAP) {
+          const float x = soft_cap(sc[r] * ta.c, ta.k2, ta.cl);
+          sc[r] = ALIBI ? x + b[r - r0] : x;
+        } else if constexpr (ALIBI) {
+          sc[r] = __builtin_fmaf(sc[r], ta.c, b[r - r0]);
+        }
         if constexpr (MASKED) {
           if (kconst(r) > ta.lim) sc[r] = kNegInf;
         }
@@ -422,7 +431,7 @@ struct Prefill {
   // reference maximum by more than the lazy threshold?  (Then the tile's P,
   // computed against the old reference, must be recomputed: see resolve.)
   static __device__ __forceinline__ bool exceeds(const State& st, const TileArgs& ta) {
-    const float ce = ALIBI ? 1.f : ta.c;
+    const float ce = LOG2 ? 1.f : ta.c;
     return __builtin_fmaf(ta.t, ce, -st.mc) > kLazyThreshold;
   }
 
@@ -435,8 +444,8 @@ struct Prefill {
   // and the tile's P is recomputed.  Rows that did not move keep their
   // reference and factor 1.
   static __device__ __forceinline__ void resolve(State& st, Scores& sc, Probs& pr, TileArgs& ta) {
-    typedef SoftPlan<false, false, ALIBI> P;
-    const float ce = ALIBI ? 1.f : ta.c;
+    typedef SoftPlan<false, false, ALIBI, CAP> P;
+    const float ce = LOG2 ? 1.f : ta.c;
     const float tm = max_halves(ta.t);
     const float d = __builtin_fmaf(tm, ce, -st.mc);
     const bool move = d > kLazyThreshold;
@@ -488,8 +497,8 @@ struct Prefill {
                                                const T* kln, const T* vl, const T* vln, const Addr& ad,
                                                TileArgs& ta, CP&& copy) {
     constexpr bool MASKED = SM == 2;
-    constexpr bool PREP = ALIBI || MASKED;
-    typedef SoftPlan<PREP, MASKED, ALIBI> P;
+    constexpr bool PREP = LOG2 || MASKED;
+    typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
     [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
       (
           [&] {
@@ -547,9 +556,9 @@ struct Prefill {
 // the inline assembly and at most 152 VGPRs.  (By itself the compiler would
 // halve the file once AGPRs are used; the build sets the kernels' AGPR
 // allocation to 104 in the device IR.)
-template <int D, typename T, bool CAUSAL, bool ALIBI>
+template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP>
 __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) void prefill_kernel(PrefillParams p) {
-  typedef Prefill<D, T, CAUSAL, ALIBI> PF;
+  typedef Prefill<D, T, CAUSAL, ALIBI, CAP> PF;
   constexpr bool REV = ALIBI;
   typedef typename PF::State State;
   typedef typename PF::Scores Scores;
@@ -761,6 +770,8 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     TileArgs ta;
     ta.c = p.c;
     ta.sl2 = ALIBI ? p.slopes[cur.hq] * kLog2e : 0.f;
+    ta.k2 = p.cap_k2;
+    ta.cl = p.cap_cl;
     ta.t = kNegInf;
     // Per-tile softmax parameters of tile(j).
     auto set_tile = [&](int j) __attribute__((always_inline)) {
@@ -912,7 +923,7 @@ int compute_units() {
   return n;
 }
 
-template <int D, typename T, bool CAUSAL, bool ALIBI>
+template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP>
 hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
   PrefillParams q = p;
   // Query heads per workgroup: the largest power of two (up to the wave
@@ -926,16 +937,19 @@ hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
   if (q.nitems == 0) return hipSuccess;
   const int grid = std::min(q.nitems, compute_units());
   q.nxcd = grid % kXcds == 0 ? kXcds : 1;
-  hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI>), dim3(grid), dim3(kThreads), 0, stream, q);
+  hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI, CAP>), dim3(grid), dim3(kThreads), 0, stream, q);
   return hipGetLastError();
 }
 
 template <int D, typename T>
 hipError_t launch_d(const PrefillParams& p, hipStream_t s) {
+  // SoftCap is built for the causal mask without ALiBi (the SoftCap operator);
+  // the entry point rejects the other combinations.
+  if (p.cap_cl != 0.f) return launch_t<D, T, true, false, true>(p, s);
   if (p.causal) {
-    return p.slopes ? launch_t<D, T, true, true>(p, s) : launch_t<D, T, true, false>(p, s);
+    return p.slopes ? launch_t<D, T, true, true, false>(p, s) : launch_t<D, T, true, false, false>(p, s);
   }
-  return p.slopes ? launch_t<D, T, false, true>(p, s) : launch_t<D, T, false, false>(p, s);
+  return p.slopes ? launch_t<D, T, false, true, false>(p, s) : launch_t<D, T, false, false, false>(p, s);
 }
 
 }  // namespace

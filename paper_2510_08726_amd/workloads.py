@@ -44,7 +44,8 @@ class Workload:
 
 # The six shapes the headline metric is quoted on, then ALiBi decode (the MHA
 # decode shape with the ALiBi bias) and SoftCap decode (Gemma 2 27B's
-# attention: 32 query heads on 16 KV heads of dim 128, logits capped at 50).
+# attention: 32 query heads on 16 KV heads of dim 128, logits capped at 50), and
+# SoftCap causal prefill with the same heads.
 # Prefill: Lq == Lk.  Decode: one query token (Lq = 1) against a KV cache of
 # Lk keys.
 WORKLOADS = {
@@ -65,6 +66,8 @@ WORKLOADS = {
                              alibi=True, decode=True, seed=7),
     "softcap_decode": Workload("softcap_decode", 16, 32, 16, 1, 8192, 128, "f16",
                                decode=True, seed=8, softcap=50.0),
+    "softcap_causal_prefill": Workload("softcap_causal_prefill", 2, 32, 16, 4096, 4096,
+                                       128, "f16", causal=True, seed=9, softcap=50.0),
 }
 
 

@@ -42,10 +42,10 @@ def assert_close(gpu_out, ref, what=""):
     return e
 
 
-def run_fwd(q, k, v, *, scale, causal=False, slopes=None):
+def run_fwd(q, k, v, *, scale, causal=False, slopes=None, softcap=None):
     dev = torch.device("cuda")
     o = pa.attn_fwd(q.to(dev), k.to(dev), v.to(dev), causal=causal, scale=scale,
-                    alibi_slopes=None if slopes is None else slopes.to(dev))
+                    alibi_slopes=None if slopes is None else slopes.to(dev), softcap=softcap)
     torch.cuda.synchronize()
     return o
 

@@ -49,8 +49,8 @@ def test_status_strings(lib):
 
 
 def fwd(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=1, Hq=2, Hkv=2, Lq=8, Lk=8, D=64, causal=0,
-        scale=0.125, slopes=NULL, dtype=0):
-    return lib.attn_fwd(q, k, v, o, B, Hq, Hkv, Lq, Lk, D, causal, scale, slopes, dtype, NULL)
+        scale=0.125, slopes=NULL, cap=0.0, dtype=0):
+    return lib.attn_fwd(q, k, v, o, B, Hq, Hkv, Lq, Lk, D, causal, scale, slopes, cap, dtype, NULL)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -61,6 +61,9 @@ def fwd(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=1, Hq=2, Hkv=2, Lq=8, Lk=8, D=64,
     (dict(Lk=-3), pa.ATTN_ERR_SHAPE), (dict(Hq=6, Hkv=4), pa.ATTN_ERR_SHAPE),
     (dict(scale=float("nan")), pa.ATTN_ERR_SHAPE), (dict(scale=float("inf")), pa.ATTN_ERR_SHAPE),
     (dict(D=96), pa.ATTN_ERR_UNSUPPORTED), (dict(D=256), pa.ATTN_ERR_UNSUPPORTED),
+    (dict(causal=1, cap=-2.0), pa.ATTN_ERR_SHAPE), (dict(causal=1, cap=float("nan")), pa.ATTN_ERR_SHAPE),
+    (dict(cap=30.0), pa.ATTN_ERR_UNSUPPORTED),                       # SoftCap without the causal mask
+    (dict(causal=1, cap=30.0, slopes=FAKE), pa.ATTN_ERR_UNSUPPORTED),  # SoftCap with ALiBi
     (dict(dtype=2), pa.ATTN_ERR_UNSUPPORTED),
     (dict(B=1 << 20, Hq=1 << 10, Hkv=1 << 10, Lq=1 << 20, Lk=1 << 20), pa.ATTN_ERR_SHAPE),
 ])

@@ -15,7 +15,7 @@ import torch
 
 import paper_2510_08726_amd as pa
 from paper_2510_08726_amd.workloads import WORKLOADS, alibi_slopes, make_inputs, random_tensors
-from gpu_common import assert_close, host32, oracle_fwd, run_fwd
+from gpu_common import assert_close, host32, host64, oracle_fwd, run_fwd
 
 pytestmark = pytest.mark.gpu
 
@@ -122,12 +122,12 @@ def test_prefill_is_deterministic():
 def _workload_run(name):
     w = WORKLOADS[name]
     q, k, v, sl = make_inputs(w)
-    o = run_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl)
+    o = run_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl, softcap=w.softcap or None)
     return w, q, k, v, sl, o.cpu()
 
 
 @pytest.mark.parametrize("name", ["tiny_noncausal", "causal_mha_prefill", "gqa_causal_prefill",
-                                  "alibi_causal_prefill"])
+                                  "alibi_causal_prefill", "softcap_causal_prefill"])
 def test_prefill_workload_sampled_rows(name):
     print(f"prefill workload {name}", flush=True)
     w, q, k, v, sl, o = _workload_run(name)
@@ -138,8 +138,47 @@ def test_prefill_workload_sampled_rows(name):
     rows = [r for r in rows if 0 <= r < L]
     heads = sorted(set([(0, 0), (w.B - 1, w.Hq - 1), (0, w.Hq // 2)]
                        + [(int(rng.integers(w.B)), int(rng.integers(w.Hq))) for _ in range(3)]))
-    ref = oracle_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl, rows=rows, heads=heads)
+    ref = oracle_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl, softcap=w.softcap or None,
+                     rows=rows, heads=heads)
     got = host32(o)[:, :, rows]
     sel_b = [b for b, _ in heads]
     sel_h = [h for _, h in heads]
     assert_close(got[sel_b, sel_h], ref[sel_b, sel_h], f"{name} sampled")
+
+
+SOFTCAP_CASES = [  # B, Hq, Hkv, Lq, Lk, D, dtype, cap, score gain
+    (1, 4, 4, 300, 300, 128, "f16", 2.0, 4.0),
+    (2, 8, 4, 257, 257, 64, "bf16", 1.0, 4.0),      # 2 query heads per KV head, ragged tail
+    (1, 16, 2, 200, 330, 128, "bf16", 5.0, 8.0),    # 8 query heads per KV head, Lq < Lk
+    (1, 2, 1, 96, 40, 64, "f16", 3.0, 4.0),         # Lq > Lk: the first rows see no key
+]
+
+
+@pytest.mark.parametrize("case", SOFTCAP_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_prefill_softcap_matches_oracle(case):
+    """Causal SoftCap prefill vs the oracle; the query is scaled up so that the
+    cap changes the result by far more than the tolerance."""
+    B, Hq, Hkv, Lq, Lk, D, dt, cap, gain = case
+    print(f"softcap prefill case {case}", flush=True)
+    q, k, v = random_tensors([(B, Hq, Lq, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], dt,
+                             seed=zlib.crc32(repr(case).encode()) % 1000)
+    q = (q.float() * gain).to(q.dtype)
+    scale = D ** -0.5
+    o = run_fwd(q, k, v, scale=scale, causal=True, softcap=cap)
+    ref = oracle_fwd(q, k, v, scale=scale, causal=True, softcap=cap)
+    assert_close(host32(o), ref, f"softcap prefill {case}")
+    plain = oracle_fwd(q, k, v, scale=scale, causal=True)
+    assert np.abs(plain - ref).max() > 0.05, "the cap must matter in this case"
+
+
+def test_prefill_softcap_last_row_equals_decode():
+    """The last query row of causal SoftCap prefill is the SoftCap decode of that token."""
+    B, Hq, Hkv, L, D, cap = 2, 8, 2, 700, 128, 2.5
+    q, k, v = random_tensors([(B, Hq, L, D), (B, Hkv, L, D), (B, Hkv, L, D)], "f16", seed=61)
+    q = (q.float() * 4).to(q.dtype)
+    o = host32(run_fwd(q, k, v, scale=D ** -0.5, causal=True, softcap=cap))
+    dev = torch.device("cuda")
+    od = pa.attn_decode(q[:, :, -1:].contiguous().to(dev), k.to(dev), v.to(dev), scale=D ** -0.5,
+                        softcap=cap, num_splits=3)
+    torch.cuda.synchronize()
+    assert_close(o[:, :, -1:], host64(od.cpu()).astype(np.float64), "prefill last row vs decode")
