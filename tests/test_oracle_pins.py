@@ -49,12 +49,13 @@ def _sdpa(q, k, v, *, scale, causal=False, slopes=None):
 # ---------------------------------------------------------------------------
 # invariants
 
-@pytest.mark.parametrize("causal,alibi", [(False, False), (True, False), (True, True)])
-def test_probability_rows_sum_to_one(causal, alibi):
+@pytest.mark.parametrize("causal,alibi,cap", [(False, False, None), (True, False, None), (True, True, None),
+                                           (True, False, 1.5), (True, True, 0.7)])
+def test_probability_rows_sum_to_one(causal, alibi, cap):
     q, k = _rand((1, 4, 37, 16), 1), _rand((1, 2, 53, 16), 2)
     sl = alibi_slopes(4).double().numpy() if alibi else None
     for hq in range(4):
-        p = oracle.softmax_probs(q, k, scale=0.25, causal=causal, alibi_slopes=sl, hq=hq)
+        p = oracle.softmax_probs(q, k, scale=0.25, causal=causal, alibi_slopes=sl, softcap=cap, hq=hq)
         assert np.all(p >= 0)
         np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-12)
         if causal:   # masked entries carry exactly zero probability
@@ -229,3 +230,16 @@ def test_golden_fixtures():
         v = np.array(c["v"], dtype=np.float64)[None, None]
         o = oracle.attention(q, k, v, scale=c["scale"], causal=c.get("causal", False))
         np.testing.assert_allclose(o[0, 0], np.array(c["o"]), atol=1e-15, err_msg=c["name"])
+
+
+def test_softcap_bounds_the_weight_ratio():
+    """|cap tanh(x / cap)| <= cap (equal once tanh rounds to 1), so without a bias
+    any two visible keys' weights differ by at most e^(2 cap), however large the
+    raw scores are."""
+    q, k = _rand((1, 2, 9, 8), 33), _rand((1, 2, 30, 8), 34)
+    cap = 1.25
+    for hq in range(2):
+        p = oracle.softmax_probs(q, k, scale=500.0, causal=True, softcap=cap, hq=hq)
+        for i in range(9):
+            row = p[i, :i + 30 - 9 + 1]
+            assert np.all(row > 0) and row.max() / row.min() <= math.exp(2 * cap) * (1 + 1e-12)
