@@ -2,8 +2,8 @@
  * attn.h — fused scaled-dot-product attention for AMD Instinct MI355X (gfx950).
  *
  * The operation is plain attention as the paper defines it (Eq. attention in
- * the appendix "Additional Example Operators" and the compute definition of the
- * appendix figure "Compute definition for the attention operator"):
+ * the appendix "Additional Example Operators", with the compute definition of
+ * Fig. appendix-attention for the product order and the rounding of exp):
  *
  *     S = Q K^T * scale + bias          (masked entries are -inf)
  *     O = softmax_rows(S) V             (exp rounded to the input dtype before P.V)

@@ -10,9 +10,9 @@ which holds none of the method's arithmetic.
 Contents
 --------
 ``attention``      the plain, unfused definition of attention (Eq. attention in
-                   the appendix "Additional Example Operators", together with
-                   the compute definition of the appendix figure "Compute
-                   definition for the attention operator").  It materialises
+                   the appendix "Additional Example Operators", with the mask
+                   and bias of the operator table and the product order of
+                   Fig. appendix-attention).  It materialises
                    the full score matrix S and the probability matrix P in
                    float64.  This is what every GPU result is compared with.
 ``rolling``        the rolling-update algorithm (Section "Rolling Update",

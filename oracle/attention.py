@@ -1,26 +1,27 @@
 """Plain, unfused float64 attention — the oracle (test infrastructure only).
 
-Follows, step by step and in the same order, the paper's compute definition
-of attention (appendix figure "Compute definition for the attention operator")
-and Eq. attention of the appendix "Additional Example Operators":
+This module is the checker of the GPU path, never part of it.  It writes out
+the definition of attention that the paper states as Eq. attention (appendix
+"Additional Example Operators"), with the mask and bias of the operators in
+the evaluation's operator table, and nothing else:
 
-    p      = q . k^T                                 (batch_matmul, trans_b)
-    score  = mask ? score_mod(p) : -inf              (if_then_else)
-    m_i    = max_j score_ij                          (softmax_maxelem)
-    e_ij   = exp(score_ij - m_i)                     (softmax_exp)
-    s_i    = sum_j e_ij                              (softmax_expsum)
-    o_id   = sum_j e_ij v_jd                         (second batch_matmul)
-    o'_id  = o_id / s_i                              (softmax_norm)
+    raw scores     r_ij = sum_d q_id k_jd
+    modified       z_ij = r_ij * scale (capped by SoftCap, plus the ALiBi bias)
+                   where key j is visible to row i, else -inf
+    weights        w_ij = exp(z_ij - max_j' z_ij')       (max shift for range)
+    output         o_id = sum_j w_ij v_jd / sum_j w_ij
 
-Everything is float64; the fp16/bf16 inputs are upcast exactly by the caller.
-The score matrix S and the matrix E (and P = E / s) are materialised in full
-for each (batch, query head): nothing is blocked, fused or reordered.
+The max shift cancels in the ratio; it only keeps exp in range.  Everything is
+float64; the fp16/bf16 inputs are upcast exactly by the caller.  The full
+score matrix and the full weight matrix of each (batch, query head) are
+materialised: nothing is blocked, fused or reordered.
 
 Readings taken where the paper is silent or garbled (each one is listed in the
 design notes):
 
 * Eq. attention prints the first product as q . v; the compute definition
-  multiplies q by k transposed, which is what is used here.
+  of Fig. appendix-attention multiplies q by k transposed, which is what is
+  used here.
 * ``score_mod(p) = p * scale + bias``: the scale multiplies q.k only and the
   bias is added after scaling.  ``scale`` is an argument (1/sqrt(D) in every
   workload).
@@ -78,7 +79,7 @@ def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, b=0,
     i = np.arange(Lq) if rows is None else np.asarray(rows, dtype=np.int64)
     qi = np.asarray(q[b, hq], dtype=np.float64)[i]          # [R, D]
     kk = np.asarray(k[b, hk], dtype=np.float64)              # [Lk, D]
-    p = qi @ kk.T                                            # batch_matmul(q, k, trans_b)
+    p = qi @ kk.T                                            # raw scores r = q k^T
     i_abs = i[:, None] + (Lk - Lq)                           # bottom-right aligned row index
     j = np.arange(Lk)[None, :]
     score = p * float(scale)
@@ -94,14 +95,14 @@ def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, b=0,
 
 def softmax_probs(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None,
                   b=0, hq=0, rows=None):
-    """Probability matrix P = e / s of one (batch, query head), materialised."""
+    """Weight matrix w / sum(w) of one (batch, query head), materialised."""
     score = scores(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes,
                    softcap=softcap, b=b, hq=hq, rows=rows)
-    m = score.max(axis=1, keepdims=True)                     # softmax_maxelem
+    m = score.max(axis=1, keepdims=True)                     # row max (shift)
     empty = ~np.isfinite(m)
     m = np.where(empty, 0.0, m)
-    e = np.exp(score - m)                                    # softmax_exp
-    s = e.sum(axis=1, keepdims=True)                         # softmax_expsum
+    e = np.exp(score - m)                                    # unnormalised weights
+    s = e.sum(axis=1, keepdims=True)                         # row sum of the weights
     return np.where(empty, 0.0, e / np.where(empty, 1.0, s))
 
 
@@ -127,12 +128,12 @@ def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, softcap=None,
         score = scores(q, k, scale=scale, causal=causal,
                        alibi_slopes=alibi_slopes, softcap=softcap, b=b, hq=hq,
                        rows=rows)
-        m = score.max(axis=1, keepdims=True)                 # softmax_maxelem
+        m = score.max(axis=1, keepdims=True)                 # row max (shift)
         empty = ~np.isfinite(m)                              # row sees no key
         m = np.where(empty, 0.0, m)
-        e = np.exp(score - m)                                # softmax_exp
-        s = e.sum(axis=1, keepdims=True)                     # softmax_expsum
-        o = e @ np.asarray(v[b, hq // group], dtype=np.float64)  # batch_matmul(e, v)
-        o = o / np.where(empty, 1.0, s)                      # softmax_norm
+        e = np.exp(score - m)                                # unnormalised weights
+        s = e.sum(axis=1, keepdims=True)                     # row sum of the weights
+        o = e @ np.asarray(v[b, hq // group], dtype=np.float64)  # weighted sum of V rows
+        o = o / np.where(empty, 1.0, s)                      # divide by the row sum
         out[b, hq] = np.where(empty, 0.0, o)
     return out

@@ -3,14 +3,16 @@
 // the plain attention definition, with the tile structure of the appendix
 // "Privatization" (a local max per key tile, then the running max).
 //
-// Work split.  One workgroup = 8 wave64s, two per SIMD, each owning 32 query
-// rows of one query head for the whole key loop: 256 rows of one (batch,
+// Work split.  One workgroup = 4 wave64s, one per SIMD, each owning 32 query
+// rows of one query head for the whole key loop: 128 rows of one (batch,
 // query head), or, when several query heads share a KV head (GQA), the same
-// 256 / hg rows of hg such heads, so that every wave sees the same keys (no
+// 128 / hg rows of hg such heads, so that every wave sees the same keys (no
 // wave idles while the others finish their causal diagonal) and all of them
-// read the same K and V tiles.  Key tiles are BN = 32 keys.  Every wave runs
-// the whole loop body for its rows, software-pipelined over three tiles:
-// iteration j
+// read the same K and V tiles.  Two such workgroups share each compute unit
+// (two waves per SIMD): they run independently, so one's barrier waits,
+// per-item setup and output overlap the other's key loop.  Key tiles are
+// BN = 32 keys.  Every wave runs the whole loop body for its rows,
+// software-pipelined over three tiles: iteration j
 //
 //   S^T(j+1) = K_{j+1} . Q^T          8 (D = 128) 32x32x16 MFMAs, K from LDS,
 //                                      Q in AGPRs
@@ -38,8 +40,9 @@
 // The K and V tiles of the workgroup pass through LDS rings of kRing slots,
 // filled by buffer loads with the LDS bit (HBM -> LDS without VGPRs) that all
 // waves issue, kRing - 1 tiles ahead of their use; one barrier per iteration
-// publishes them.  Each wave also owns one LDS tile through which its Q rows
-// come in and its O rows go out, as whole 1 KB blocks.
+// publishes them.  Between work items each wave borrows one ring slot that
+// the next item's first copies leave free: its O rows go out and its next
+// Q rows come in through it, as whole 1 KB blocks.
 //
 // The MFMAs are written as inline assembly to fix their register files: the
 // S^T accumulators in VGPRs (the softmax reads them), Q, O^T and l in fixed
@@ -67,12 +70,17 @@ namespace attn {
 
 namespace {
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kWgPerCu = 2;                 // resident workgroups per compute unit
 constexpr int BMW = 32;                     // query rows per wave
 constexpr int BM = BMW * kWaves;            // query rows per workgroup of one head
 constexpr int BN = 32;                      // keys per tile
 constexpr int kRing = 4;                    // LDS slots per operand; copies run kRing - 1 tiles ahead
+static_assert(kRing >= 4, "the first V tiles are staged before the item, the rest copied kRing - 2 ahead");
+// The key loop is unrolled so that ring slots and the parity of the score
+// buffers are compile-time choices.
+constexpr int kUnroll = kRing % 2 == 0 ? kRing : 2 * kRing;
 // A row's reference maximum moves only when a tile's maximum exceeds it by
 // more than this (log2 units), so that P <= 2^kLazyThreshold.
 constexpr float kLazyThreshold = 8.f;
@@ -552,12 +560,12 @@ struct Prefill {
   }
 };
 
-// Two waves per SIMD leave each wave 256 registers: the 102 AGPRs named by
-// the inline assembly and at most 152 VGPRs.  (By itself the compiler would
-// halve the file once AGPRs are used; the build sets the kernels' AGPR
-// allocation to 104 in the device IR.)
+// Two waves per SIMD (two workgroups per compute unit) leave each wave 256
+// registers: the 102 AGPRs named by the inline assembly and at most 152
+// VGPRs.  (By itself the compiler would halve the file once AGPRs are used;
+// the build sets the kernels' AGPR allocation to 104 in the device IR.)
 template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP>
-__global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) void prefill_kernel(PrefillParams p) {
+__global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(152))) void prefill_kernel(PrefillParams p) {
   typedef Prefill<D, T, CAUSAL, ALIBI, CAP> PF;
   constexpr bool REV = ALIBI;
   typedef typename PF::State State;
@@ -571,10 +579,9 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
   constexpr int NB = PF::NB;
   constexpr int CPW = PF::CPW;
   constexpr int CPR = PF::CPR;
-  // LDS: a ring of kRing K tiles, a ring of kRing V tiles, then one tile
-  // per wave that stages the wave's 32 O rows out at the end of a work item,
-  // in the layout of the K and V tiles.
-  __shared__ __attribute__((aligned(1024))) T lds[(2 * kRing + kWaves) * TE];
+  // LDS: a ring of kRing K tiles and a ring of kRing V tiles (64 KB for
+  // D = 128, so that two workgroups fit a compute unit).
+  __shared__ __attribute__((aligned(1024))) T lds[2 * kRing * TE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -670,11 +677,17 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
   PF::make_addr(ad, lane);
 
   // This wave's staging tile: Q rows in at the start of a work item, O rows
-  // out at its end.
-  const T* xl = lds + (2 * kRing + wave) * TE;
-  const uint32_t xslot = lds0 + (uint32_t)((2 * kRing + wave) * TE * (int)sizeof(T));
-  // The first tiles of a work item: K tiles 0 .. kRing-2 and V tile 0, each
-  // wave its blocks.  Issued once the previous item's last barrier has
+  // out at its end.  It is a ring slot that the first copies of a work item
+  // (K slots 0 .. kRing-2, V slots 0 .. kRing-4, issued by stage_kv) leave
+  // free: K slot kRing-1 for wave 0, V slot kRing-4+w for wave w >= 1.  The
+  // ring takes it back in the item's first iterations, after the barrier
+  // that follows the Q reads.
+  static_assert(kWaves == 4, "three free V slots and one free K slot between work items");
+  const int xs = wave == 0 ? kRing - 1 : kRing + kRing - 4 + wave;
+  const T* xl = lds + xs * TE;
+  const uint32_t xslot = lds0 + (uint32_t)(xs * TE * (int)sizeof(T));
+  // The first tiles of a work item: K tiles 0 .. kRing-2 and V tiles
+  // 0 .. kRing-4, each wave its blocks.  Issued once the previous item's last barrier has
   // passed (every ring slot is free then), before that item's output.
   auto stage_kv = [&](const Item& it) __attribute__((always_inline)) {
     const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)it.kvh * Lk * D;
@@ -686,7 +699,8 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
 #pragma unroll
         for (int t = 0; t < kRing - 1; ++t) PF::copy_block(kp, it.rows, kslot(t), tile_of(it, t), b, dof[u]);
       } else {
-        PF::copy_block(vp, it.rows, vslot(0), tile_of(it, 0), b, dof[u]);
+#pragma unroll
+        for (int t = 0; t < kRing - 3; ++t) PF::copy_block(vp, it.rows, vslot(t), tile_of(it, t), b, dof[u]);
       }
     }
   };
@@ -723,22 +737,22 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     auto tile = [&](int j) __attribute__((always_inline)) { return tile_of(cur, j); };
     // Copy u of this wave in iteration j: its block of K tile(j + kRing) into
     // K slot j mod kRing (whose tile j was last read in iteration j - 1), or
-    // of V tile(j + kRing - 2) into V slot (j + 2) mod kRing (whose tile j - 2
+    // of V tile(j + kRing - 2) into V slot (j - 2) mod kRing (whose tile j - 2
     // was last read in iteration j - 1), anywhere in the iteration.
     auto copy = [&](int j, auto slotc, auto uc) __attribute__((always_inline)) {
-      constexpr int k = decltype(slotc)::value;
+      constexpr int k = decltype(slotc)::value % kRing;
       constexpr int u = decltype(uc)::value;
       const int b = (u * kWaves + wave) % NB;
       if (PF::copies_k(u, wave)) PF::copy_block(kp, cur.rows, kslot(k), tile(j + kRing), b, dof[u]);
-      else PF::copy_block(vp, cur.rows, vslot((k + 2) % kRing), tile(j + kRing - 2), b, dof[u]);
+      else PF::copy_block(vp, cur.rows, vslot((k + kRing - 2) % kRing), tile(j + kRing - 2), b, dof[u]);
     };
     // Iterations j in [j0, j1), j0 >= -1, of one variant; the loop body is
-    // unrolled by kRing so that slots and parities are compile-time choices.
+    // unrolled by kUnroll so that slots and parities are compile-time choices.
     // Every iteration ends in one barrier, so the waves of the workgroup stay
     // in step whatever their phase boundaries.
     auto phase = [&](auto& iteration, int j0, int j1, auto var) __attribute__((always_inline)) {
-      for (int jb = j0 & ~(kRing - 1); jb < j1; jb += kRing) {
-        static_for<kRing>([&](auto kc) __attribute__((always_inline)) {
+      for (int jb = j0 - ((j0 % kUnroll) + kUnroll) % kUnroll; jb < j1; jb += kUnroll) {
+        static_for<kUnroll>([&](auto kc) __attribute__((always_inline)) {
           const int j = jb + decltype(kc)::value;
           if (j >= j0 && j < j1) iteration(j, var, kc);
         });
@@ -800,9 +814,9 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     // the threshold in some row of the wave.  A tile's first fragments are
     // read at the end of the iteration before its use, so its copy, issued
     // kRing - 1 iterations before its use, must be complete at the barrier
-    // that ends the iteration two before its use: vmcnt lets only the current
-    // iteration's copies stay in flight (every iteration issues the same
-    // number of copies), and lgkmcnt lets the reads of the next iteration's
+    // that ends the iteration two before its use: vmcnt lets the copies of
+    // the last kRing - 3 iterations stay in flight (every iteration issues
+    // the same number of copies), and lgkmcnt lets the reads of the next iteration's
     // first fragments, which touch neither slot copied into next, cross the
     // barrier.
     auto iteration = [&](int j, auto var, auto slotc) __attribute__((always_inline)) {
@@ -810,8 +824,8 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
       constexpr bool QK = (VAR & 1) != 0;
       constexpr int SM = (VAR >> 1) & 3;
       constexpr bool PV = (VAR & 8) != 0;
-      constexpr int k = decltype(slotc)::value;     // j mod kRing
-      constexpr int par = k & 1;
+      constexpr int par = decltype(slotc)::value & 1;   // j mod 2
+      constexpr int k = decltype(slotc)::value % kRing;   // j mod kRing
       const T* kl_use = lds + ((k + 1) % kRing) * TE;                   // K_{j+1}
       const T* kl_nxt = lds + ((k + 2) % kRing) * TE;                   // K_{j+2}
       const T* vl_use = lds + (kRing + (k + kRing - 1) % kRing) * TE;   // V_{j-1}
@@ -829,7 +843,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
       // iteration's first reads of their results; this iteration's copies
       // may stay in flight; then the barrier.
       asm volatile("s_nop 7\n\ts_nop 7\n\ts_waitcnt vmcnt(%0) lgkmcnt(%1)\n\ts_barrier"
-                   : : "n"(CPW), "n"(PF::kPrime) : "memory");
+                   : : "n"((kRing - 3) * CPW), "n"(PF::kPrime) : "memory");
     };
     constexpr int PRO = 1, EPI = 8;
     constexpr int FIRST_WHOLE = 1 + 2, FIRST_MASKED = 1 + 4;
@@ -849,7 +863,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
       phase(iteration, nt, nt + 1, std::integral_constant<int, EPI>{});
     } else {
       // Visible tiles 0 .. n_w - 1 at iterations 0 .. n_w - 1, masked ones last.
-      iteration(-1, std::integral_constant<int, PRO>{}, std::integral_constant<int, kRing - 1>{});
+      iteration(-1, std::integral_constant<int, PRO>{}, std::integral_constant<int, kUnroll - 1>{});
       if (fm_w > 0) iteration(0, std::integral_constant<int, FIRST_WHOLE>{}, std::integral_constant<int, 0>{});
       else iteration(0, std::integral_constant<int, FIRST_MASKED>{}, std::integral_constant<int, 0>{});
       phase(iteration, 1, fm_w, std::integral_constant<int, WHOLE>{});
@@ -863,6 +877,10 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
     hazard_pad();
     keep_live(sc[0]);
     keep_live(sc[1]);
+    // The last iterations' copies (of tiles past the item, which write
+    // zeros) may still be in flight into the slots that stage the output:
+    // every wave waits for its own, then the barrier.
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
 
     Item nxt;
     const bool more = item_at(round + 1, nxt);
@@ -910,7 +928,7 @@ __global__ __launch_bounds__(kThreads, 1) __attribute__((amdgpu_num_vgpr(152))) 
   }
 }
 
-// Compute units of the current device: one persistent workgroup each.
+// Compute units of the current device: kWgPerCu persistent workgroups each.
 int compute_units() {
   static std::atomic<int> cached[64];
   int dev = 0;
@@ -935,7 +953,7 @@ hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
   q.nheads = p.B * p.Hq;
   q.nitems = q.nqb * (q.nheads / q.hg);
   if (q.nitems == 0) return hipSuccess;
-  const int grid = std::min(q.nitems, compute_units());
+  const int grid = std::min(q.nitems, kWgPerCu * compute_units());
   q.nxcd = grid % kXcds == 0 ? kXcds : 1;
   hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI, CAP>), dim3(grid), dim3(kThreads), 0, stream, q);
   return hipGetLastError();
