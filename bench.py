@@ -134,12 +134,13 @@ def run_workload(name, steps, warmup):
 
         def fn():
             pa.attn_fwd(q, k, v, o, causal=w.causal, scale=w.sm_scale, alibi_slopes=sl,
-                        softcap=w.softcap or None)
-        work = prefill_flops(w.B, w.Hq, w.Lq, w.Lk, w.D, w.causal)
+                        softcap=w.softcap or None, window=w.window or None)
+        work = prefill_flops(w.B, w.Hq, w.Lq, w.Lk, w.D, w.causal, w.window)
     ms, wall_ms = time_steps(fn, steps, warmup)
     res = {
         "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk, "D": w.D, "dtype": w.dtype,
-        "causal": w.causal, "alibi": w.alibi, "softcap": w.softcap, "ms_per_step": round(ms, 5),
+        "causal": w.causal, "alibi": w.alibi, "softcap": w.softcap, "window": w.window,
+        "ms_per_step": round(ms, 5),
         "host_wall_ms_per_step": round(wall_ms, 5),
     }
     if w.decode:

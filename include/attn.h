@@ -65,9 +65,11 @@ typedef enum {
   ATTN_OK = 0,
   ATTN_ERR_NULL = -1,        /* a required pointer is NULL */
   ATTN_ERR_SHAPE = -2,       /* a size is < 1, Hq % Hkv != 0, num_splits < 0, a size overflows,
-                                scale is not finite, or softcap is negative or not finite */
-  ATTN_ERR_UNSUPPORTED = -3, /* head dim not 64 or 128, unknown dtype, or (attn_fwd) softcap
-                                without the causal mask or together with ALiBi */
+                                scale is not finite, softcap is negative or not finite, or
+                                window is negative */
+  ATTN_ERR_UNSUPPORTED = -3, /* head dim not 64 or 128, unknown dtype, or (attn_fwd_mod)
+                                softcap or window without the causal mask, or softcap
+                                together with ALiBi */
   ATTN_ERR_WORKSPACE = -4,   /* decode workspace smaller than attn_decode_workspace_bytes() */
   ATTN_ERR_HIP = -5          /* a HIP launch failed; see attn_last_hip_error() */
 } attn_status;
@@ -80,18 +82,40 @@ typedef enum {
  *   causal  0 or 1 (non-zero means 1)
  *   scale   finite float
  *   alibi_slopes  device float[Hq] or NULL
- *   softcap 0 for none, or cap > 0 (causal and without ALiBi only): each
- *           scaled score becomes cap * tanh(score * scale / cap) before the
- *           mask, as described for attn_decode
  *
- * Errors: ATTN_ERR_NULL if Q, K, V or O is NULL; ATTN_ERR_SHAPE for bad sizes
- * or a negative / non-finite softcap; ATTN_ERR_UNSUPPORTED for D, dtype, or
- * softcap without causal or with ALiBi; ATTN_ERR_HIP if the launch fails.
+ * Errors: ATTN_ERR_NULL if Q, K, V or O is NULL; ATTN_ERR_SHAPE for bad sizes;
+ * ATTN_ERR_UNSUPPORTED for D or dtype; ATTN_ERR_HIP if the launch fails.
  */
 int attn_fwd(const void* Q, const void* K, const void* V, void* O,
              int B, int Hq, int Hkv, int Lq, int Lk, int D,
-             int causal, float scale, const float* alibi_slopes, float softcap,
+             int causal, float scale, const float* alibi_slopes,
              attn_dtype dtype, hipStream_t stream);
+
+/*
+ * attn_fwd with the score modifiers of the paper's operator table (Table
+ * tab:operators) that go beyond causal masking and ALiBi.  softcap = 0 and
+ * window = 0 make it exactly attn_fwd.
+ *
+ *   softcap 0 for none, or cap > 0 (causal only, without ALiBi): the SoftCap
+ *           operator (attention with a SoftCap score modifier, GQA heads and
+ *           the causal mask, from Gemma 2; the formula is not printed): each
+ *           scaled score becomes cap * tanh(score * scale / cap) before the
+ *           mask.
+ *   window  0 for none, or W >= 1 (causal only): the Window operator
+ *           (attention with a windowed mask, from Gemma 2), read as Gemma 2's
+ *           causal sliding window: query row i sees key j iff
+ *           i + (Lk - Lq) - W < j <= i + (Lk - Lq), i.e. its last W keys.
+ *           W >= Lk is plain causal attention; W = 1 selects V[i + Lk - Lq].
+ *           It combines with ALiBi and with softcap.
+ *
+ * Errors: as attn_fwd, plus ATTN_ERR_SHAPE for a negative or non-finite
+ * softcap or a negative window, and ATTN_ERR_UNSUPPORTED for softcap or
+ * window without the causal mask, or softcap together with ALiBi.
+ */
+int attn_fwd_mod(const void* Q, const void* K, const void* V, void* O,
+                 int B, int Hq, int Hkv, int Lq, int Lk, int D,
+                 int causal, float scale, const float* alibi_slopes, float softcap, int window,
+                 attn_dtype dtype, hipStream_t stream);
 
 /*
  * Bytes of decode workspace needed for (B, Hq, D, num_splits), num_splits >= 1
@@ -125,11 +149,6 @@ int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D);
  *   Q [B, Hq, 1, D], K and V [B, Hkv, Lk, D], O [B, Hq, 1, D]   (device)
  *   The query is the token at position Lk - 1, so every key is visible (the
  *   causal mask is a no-op).  alibi_slopes as for attn_fwd, with i = Lk - 1.
- *   softcap     0 for none, or cap > 0: the SoftCap operator of the paper's
- *               evaluation (its operator table: attention with a SoftCap
- *               score modifier, GQA heads and the causal mask, from Gemma 2;
- *               the formula is not printed).  Each scaled score becomes
- *               cap * tanh(score * scale / cap) before the ALiBi bias is added.
  *   num_splits  >= 1 chunks of ceil(Lk / num_splits) keys (the last chunk may
  *               be short, chunks past Lk are empty), or 0 for the heuristic.
  *   workspace   device buffer of at least attn_decode_workspace_bytes(B, Hq,
@@ -142,9 +161,47 @@ int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D);
  */
 int attn_decode(const void* Q, const void* K, const void* V, void* O,
                 int B, int Hq, int Hkv, int Lk, int D,
-                float scale, const float* alibi_slopes, float softcap, int num_splits,
+                float scale, const float* alibi_slopes, int num_splits,
                 void* workspace, size_t workspace_bytes,
                 attn_dtype dtype, hipStream_t stream);
+
+/*
+ * attn_decode with the SoftCap score modifier (softcap = 0 makes it exactly
+ * attn_decode):
+ *   softcap     0 for none, or cap > 0: the SoftCap operator of the paper's
+ *               operator table (Table tab:operators); each scaled score
+ *               becomes cap * tanh(score * scale / cap) before the ALiBi bias
+ *               is added.
+ * Errors: as attn_decode, plus ATTN_ERR_SHAPE for a negative or non-finite
+ * softcap.
+ */
+int attn_decode_mod(const void* Q, const void* K, const void* V, void* O,
+                    int B, int Hq, int Hkv, int Lk, int D,
+                    float scale, const float* alibi_slopes, float softcap, int num_splits,
+                    void* workspace, size_t workspace_bytes,
+                    attn_dtype dtype, hipStream_t stream);
+
+/*
+ * The kernels that attn_fwd_mod (attn_fwd: softcap = 0, window = 0) launches
+ * for these arguments, written to buf as a NUL-terminated string such as
+ * "prefill_kernel<128,f16,1,0,0,0>" (head dim, element type, then the
+ * causal, ALiBi, SoftCap and window template flags).  Host only: no HIP call.
+ * For coverage checks and profiles of the rolling-update kernel (Section
+ * "Rolling Update").  alibi: non-zero if slopes would be passed.
+ * Errors: the argument errors of attn_fwd_mod; ATTN_ERR_SHAPE if buf is NULL
+ * or shorter than the name.
+ */
+int attn_fwd_kernels(int D, attn_dtype dtype, int causal, int alibi, float softcap, int window,
+                     char* buf, size_t len);
+
+/*
+ * The kernels that attn_decode_mod (attn_decode: softcap = 0) launches, as
+ * "split;combine" with the template arguments, e.g.
+ * "decode_mfma_kernel<128,f16,0,0>;decode_combine_kernel<128,f16>" (local
+ * and global nests of Fig. su-result).  Host only.  Errors as
+ * attn_fwd_kernels.
+ */
+int attn_decode_kernels(int Hq, int Hkv, int D, attn_dtype dtype, int alibi, float softcap, char* buf, size_t len);
 
 /* Static, human-readable name of an attn_status value. */
 const char* attn_status_string(int status);

@@ -35,6 +35,11 @@ design notes):
   hq // (Hq // Hkv) (contiguous groups).
 * ALiBi: bias_ij = -slope[hq] * (i_abs - j) with i_abs = i + (Lk - Lq).  The
   slopes are an input; the oracle takes whatever values the GPU receives.
+* Window (the operator table lists it as attention with a windowed mask,
+  taken from Gemma 2 27B; the width is not printed): Gemma 2's causal
+  sliding window of ``window`` keys.  Row i sees key j iff
+  i_abs - window < j <= i_abs; it needs the causal mask.  None or 0 means no
+  window.
 * SoftCap (the operator table of the evaluation lists it as attention with a
   SoftCap score modifier, GQA heads and the causal mask, taken from Gemma 2
   27B; the paper prints no formula): the scaled product is capped smoothly,
@@ -64,8 +69,8 @@ def _softcap(x, cap):
     return cap * np.tanh(x / cap)
 
 
-def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, b=0,
-           hq=0, rows=None):
+def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, window=None,
+           b=0, hq=0, rows=None):
     """Score matrix of one (batch, query head): score_mod(q.k^T) or -inf.
 
     Returns an array [len(rows), Lk] of float64.  ``rows`` selects query rows
@@ -90,14 +95,18 @@ def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, b=0,
         score = score + (-slope) * (i_abs - j)
     if causal:
         score = np.where(j <= i_abs, score, -np.inf)
+    if window:
+        if not causal:
+            raise ValueError("the sliding window is defined with the causal mask")
+        score = np.where(j > i_abs - int(window), score, -np.inf)
     return score
 
 
 def softmax_probs(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None,
-                  b=0, hq=0, rows=None):
+                  window=None, b=0, hq=0, rows=None):
     """Weight matrix w / sum(w) of one (batch, query head), materialised."""
     score = scores(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes,
-                   softcap=softcap, b=b, hq=hq, rows=rows)
+                   softcap=softcap, window=window, b=b, hq=hq, rows=rows)
     m = score.max(axis=1, keepdims=True)                     # row max (shift)
     empty = ~np.isfinite(m)
     m = np.where(empty, 0.0, m)
@@ -107,13 +116,14 @@ def softmax_probs(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None,
 
 
 def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, softcap=None,
-              rows=None, heads=None):
+              window=None, rows=None, heads=None):
     """O = softmax(q.k^T * scale + bias, masked) . v, in float64.
 
     q: [B, Hq, Lq, D]; k, v: [B, Hkv, Lk, D]; numpy arrays of any real dtype,
     converted to float64 exactly one (batch, head) slice at a time.
     ``alibi_slopes``: None or [Hq] values.  ``softcap``: None/0, or the cap > 0
-    of the SoftCap score modifier.  ``rows``: optional query-row indices to
+    of the SoftCap score modifier.  ``window``: None/0, or the width W >= 1
+    of the causal sliding window.  ``rows``: optional query-row indices to
     compute (others are skipped, not approximated); ``heads``: optional list
     of (b, hq) pairs to compute.
     Returns float64 [B, Hq, R, D] where R = Lq or len(rows); rows of skipped
@@ -126,8 +136,8 @@ def attention(q, k, v, *, scale, causal=False, alibi_slopes=None, softcap=None,
     todo = [(b, h) for b in range(B) for h in range(Hq)] if heads is None else heads
     for b, hq in todo:
         score = scores(q, k, scale=scale, causal=causal,
-                       alibi_slopes=alibi_slopes, softcap=softcap, b=b, hq=hq,
-                       rows=rows)
+                       alibi_slopes=alibi_slopes, softcap=softcap, window=window,
+                       b=b, hq=hq, rows=rows)
         m = score.max(axis=1, keepdims=True)                 # row max (shift)
         empty = ~np.isfinite(m)                              # row sees no key
         m = np.where(empty, 0.0, m)

@@ -30,7 +30,7 @@ def _repair(prev, cur):
 
 
 def rolling_update_attention(q, k, v, *, scale, causal=False, alibi_slopes=None,
-                             block_n=64, b=0, hq=0, trace=False):
+                             window=None, block_n=64, b=0, hq=0, trace=False):
     """Attention of one (batch, query head) by rolling update over key tiles.
 
     Returns ``o`` [Lq, D] (float64); with ``trace=True`` also a list holding,
@@ -41,7 +41,7 @@ def rolling_update_attention(q, k, v, *, scale, causal=False, alibi_slopes=None,
     group = q.shape[1] // k.shape[1]
     vv = v[b, hq // group]
     score = _scores(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes,
-                    b=b, hq=hq)                               # [Lq, Lk]
+                    window=window, b=b, hq=hq)                # [Lq, Lk]
     Lq, Lk = score.shape
     D = vv.shape[1]
     xmax_0 = np.full((Lq, 1), -np.inf)

@@ -15,7 +15,8 @@ import os
 import torch
 
 __all__ = [
-    "attn_fwd", "attn_decode", "attn_decode_workspace_bytes", "attn_decode_num_splits",
+    "attn_fwd", "attn_fwd_mod", "attn_decode", "attn_decode_mod", "attn_decode_workspace_bytes",
+    "attn_decode_num_splits", "attn_fwd_kernels", "attn_decode_kernels",
     "attn_status_string", "attn_last_hip_error", "library_path", "load_library", "AttnError",
     "ATTN_OK", "ATTN_ERR_NULL", "ATTN_ERR_SHAPE", "ATTN_ERR_UNSUPPORTED", "ATTN_ERR_WORKSPACE",
     "ATTN_ERR_HIP",
@@ -60,14 +61,22 @@ def load_library():
             "or `python paper_2510_08726_amd/build.py` first")
     lib = ctypes.CDLL(path)
     vp, ci, cf, cs = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
-    lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, vp, cf, ci, vp]
+    lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, vp, ci, vp]
     lib.attn_fwd.restype = ci
-    lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, cf, ci, vp, cs, ci, vp]
+    lib.attn_fwd_mod.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, vp, cf, ci, ci, vp]
+    lib.attn_fwd_mod.restype = ci
+    lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, ci, vp, cs, ci, vp]
     lib.attn_decode.restype = ci
+    lib.attn_decode_mod.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, cf, ci, vp, cs, ci, vp]
+    lib.attn_decode_mod.restype = ci
     lib.attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci]
     lib.attn_decode_workspace_bytes.restype = cs
     lib.attn_decode_num_splits.argtypes = [ci, ci, ci, ci, ci]
     lib.attn_decode_num_splits.restype = ci
+    lib.attn_fwd_kernels.argtypes = [ci, ci, ci, ci, cf, ci, ctypes.c_char_p, cs]
+    lib.attn_fwd_kernels.restype = ci
+    lib.attn_decode_kernels.argtypes = [ci, ci, ci, ci, ci, cf, ctypes.c_char_p, cs]
+    lib.attn_decode_kernels.restype = ci
     lib.attn_status_string.argtypes = [ci]
     lib.attn_status_string.restype = ctypes.c_char_p
     lib.attn_last_hip_error.argtypes = []
@@ -120,29 +129,51 @@ def _check_tensors(q, k, v, slopes):
         _require(slopes.numel() == q.shape[1], "alibi_slopes needs one value per query head")
 
 
-def attn_fwd(q, k, v, o=None, *, causal=False, scale=None, alibi_slopes=None, softcap=None,
-             stream=None):
-    """O = softmax(Q K^T * scale + bias) V by the fused prefill kernel.
-
-    q [B, Hq, Lq, D], k and v [B, Hkv, Lk, D] (float16 or bfloat16, contiguous,
-    on the GPU); ``o`` is written if given, else allocated.  ``scale``
-    defaults to 1/sqrt(D).  ``softcap``: None, or the cap > 0 of the SoftCap
-    score modifier (causal, without ALiBi).  Returns ``o``.
-    """
+def _fwd_args(q, k, v, o, alibi_slopes):
     _check_tensors(q, k, v, alibi_slopes)
     B, Hq, Lq, D = q.shape
-    Hkv, Lk = k.shape[1], k.shape[2]
     _require(k.shape[0] == B and k.shape[3] == D, "k/v batch and head dim must match q")
     if o is None:
         o = torch.empty_like(q)
     _require(o.shape == q.shape and o.dtype == q.dtype and o.is_contiguous() and o.is_cuda,
              "o must be a contiguous GPU tensor shaped like q")
+    return o
+
+
+def attn_fwd(q, k, v, o=None, *, causal=False, scale=None, alibi_slopes=None, softcap=None,
+             window=None, stream=None):
+    """O = softmax(Q K^T * scale + bias) V by the fused prefill kernel.
+
+    q [B, Hq, Lq, D], k and v [B, Hkv, Lk, D] (float16 or bfloat16, contiguous,
+    on the GPU); ``o`` is written if given, else allocated.  ``scale``
+    defaults to 1/sqrt(D).  ``softcap`` (cap > 0) and ``window`` (W >= 1)
+    select the score modifiers of ``attn_fwd_mod``; without them the call
+    goes to the C entry point ``attn_fwd``.  Returns ``o``.
+    """
+    if softcap or window:
+        return attn_fwd_mod(q, k, v, o, causal=causal, scale=scale, alibi_slopes=alibi_slopes,
+                            softcap=softcap, window=window, stream=stream)
+    o = _fwd_args(q, k, v, o, alibi_slopes)
+    B, Hq, Lq, D = q.shape
+    Hkv, Lk = k.shape[1], k.shape[2]
     sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
-    lib = load_library()
-    _check(lib.attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lq, Lk, D,
-                        int(bool(causal)), sc, _ptr(alibi_slopes), float(softcap or 0.0),
-                        _DTYPE_CODE[q.dtype],
-                        _stream(stream)))
+    _check(load_library().attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lq, Lk, D,
+                                   int(bool(causal)), sc, _ptr(alibi_slopes), _DTYPE_CODE[q.dtype],
+                                   _stream(stream)))
+    return o
+
+
+def attn_fwd_mod(q, k, v, o=None, *, causal=False, scale=None, alibi_slopes=None, softcap=None,
+                 window=None, stream=None):
+    """attn_fwd with the SoftCap modifier (``softcap``: None or cap > 0) and the
+    causal sliding window (``window``: None or W >= 1 keys per row)."""
+    o = _fwd_args(q, k, v, o, alibi_slopes)
+    B, Hq, Lq, D = q.shape
+    Hkv, Lk = k.shape[1], k.shape[2]
+    sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    _check(load_library().attn_fwd_mod(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lq, Lk, D,
+                                       int(bool(causal)), sc, _ptr(alibi_slopes), float(softcap or 0.0),
+                                       int(window or 0), _DTYPE_CODE[q.dtype], _stream(stream)))
     return o
 
 
@@ -154,14 +185,7 @@ def attn_decode_num_splits(B, Hq, Hkv, Lk, D):
     return load_library().attn_decode_num_splits(B, Hq, Hkv, Lk, D)
 
 
-def attn_decode(q, k, v, o=None, *, scale=None, alibi_slopes=None, softcap=None, num_splits=0,
-                workspace=None, stream=None):
-    """Single-token decode by split-k: q [B, Hq, 1, D] against k, v [B, Hkv, Lk, D].
-
-    ``softcap``: None, or the cap > 0 of the SoftCap score modifier
-    (cap * tanh(scale q.k / cap)).  ``num_splits`` = 0 lets the library choose.  ``workspace`` (uint8 GPU
-    tensor) is allocated when not given.  Returns ``o`` [B, Hq, 1, D].
-    """
+def _decode_args(q, k, v, o, alibi_slopes, num_splits, workspace):
     _check_tensors(q, k, v, alibi_slopes)
     B, Hq, Lq, D = q.shape
     _require(Lq == 1, "decode takes one query token (q.shape[2] == 1)")
@@ -176,12 +200,60 @@ def attn_decode(q, k, v, o=None, *, scale=None, alibi_slopes=None, softcap=None,
     need = lib.attn_decode_workspace_bytes(B, Hq, D, max(S, 1))
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    return o, workspace
+
+
+def attn_decode(q, k, v, o=None, *, scale=None, alibi_slopes=None, softcap=None, num_splits=0,
+                workspace=None, stream=None):
+    """Single-token decode by split-k: q [B, Hq, 1, D] against k, v [B, Hkv, Lk, D].
+
+    ``softcap``: None, or the cap > 0 of the SoftCap score modifier
+    (cap * tanh(scale q.k / cap)); with it the call goes to ``attn_decode_mod``.
+    ``num_splits`` = 0 lets the library choose.  ``workspace`` (uint8 GPU
+    tensor) is allocated when not given.  Returns ``o`` [B, Hq, 1, D].
+    """
+    if softcap:
+        return attn_decode_mod(q, k, v, o, scale=scale, alibi_slopes=alibi_slopes, softcap=softcap,
+                               num_splits=num_splits, workspace=workspace, stream=stream)
+    o, workspace = _decode_args(q, k, v, o, alibi_slopes, num_splits, workspace)
+    B, Hq, _, D = q.shape
+    Hkv, Lk = k.shape[1], k.shape[2]
     sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
-    _check(lib.attn_decode(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lk, D, sc,
-                           _ptr(alibi_slopes), float(softcap or 0.0), int(num_splits), _ptr(workspace),
-                           workspace.numel() * workspace.element_size(), _DTYPE_CODE[q.dtype],
-                           _stream(stream)))
+    _check(load_library().attn_decode(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lk, D, sc,
+                                      _ptr(alibi_slopes), int(num_splits), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _DTYPE_CODE[q.dtype],
+                                      _stream(stream)))
     return o
+
+
+def attn_decode_mod(q, k, v, o=None, *, scale=None, alibi_slopes=None, softcap=None, num_splits=0,
+                    workspace=None, stream=None):
+    """attn_decode with the SoftCap score modifier (``softcap``: None or cap > 0)."""
+    o, workspace = _decode_args(q, k, v, o, alibi_slopes, num_splits, workspace)
+    B, Hq, _, D = q.shape
+    Hkv, Lk = k.shape[1], k.shape[2]
+    sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    _check(load_library().attn_decode_mod(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lk, D, sc,
+                                          _ptr(alibi_slopes), float(softcap or 0.0), int(num_splits),
+                                          _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                          _DTYPE_CODE[q.dtype], _stream(stream)))
+    return o
+
+
+def attn_fwd_kernels(D, dtype, causal, alibi, softcap=0.0, window=0):
+    """Names of the kernels attn_fwd_mod launches for these arguments (host only)."""
+    buf = ctypes.create_string_buffer(256)
+    _check(load_library().attn_fwd_kernels(D, _DTYPE_CODE.get(dtype, dtype), int(bool(causal)), int(bool(alibi)),
+                                           float(softcap or 0.0), int(window or 0), buf, 256))
+    return buf.value.decode().split(";")
+
+
+def attn_decode_kernels(Hq, Hkv, D, dtype, alibi, softcap=0.0):
+    """Names of the kernels attn_decode_mod launches for these arguments (host only)."""
+    buf = ctypes.create_string_buffer(256)
+    _check(load_library().attn_decode_kernels(Hq, Hkv, D, _DTYPE_CODE.get(dtype, dtype), int(bool(alibi)),
+                                              float(softcap or 0.0), buf, 256))
+    return buf.value.decode().split(";")
 
 
 def decode_partials(workspace, B, Hq, D, num_splits):

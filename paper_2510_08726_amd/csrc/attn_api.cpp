@@ -4,6 +4,8 @@
 
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
+#include <cstring>
 #include <limits>
 
 #include "../../include/attn.h"
@@ -50,11 +52,19 @@ int compute_units() {
   return n;
 }
 
-int gqa_heads_per_block(int group) {
-  if (group % 8 == 0) return 8;
-  if (group % 4 == 0) return 4;
-  if (group % 2 == 0) return 2;
-  return 1;
+// Query heads that one decode workgroup serves (the grid divides the group by it).
+int decode_heads_per_block(int group) {
+  const int gh = attn::decode_split_heads(group);
+  return gh == 0 ? group : gh;
+}
+
+const char* dtype_name(attn_dtype dtype) { return dtype == ATTN_BF16 ? "bf16" : "f16"; }
+
+int put(char* buf, size_t len, const char* s) {
+  const size_t n = std::strlen(s);
+  if (!buf || n + 1 > len) return ATTN_ERR_SHAPE;
+  std::memcpy(buf, s, n + 1);
+  return ATTN_OK;
 }
 
 }  // namespace
@@ -65,8 +75,8 @@ const char* attn_status_string(int status) {
   switch (status) {
     case ATTN_OK: return "ATTN_OK: success";
     case ATTN_ERR_NULL: return "ATTN_ERR_NULL: a required pointer is NULL";
-    case ATTN_ERR_SHAPE: return "ATTN_ERR_SHAPE: invalid sizes (need B,Hq,Hkv,Lq,Lk >= 1, Hq % Hkv == 0, num_splits >= 0, finite scale)";
-    case ATTN_ERR_UNSUPPORTED: return "ATTN_ERR_UNSUPPORTED: head dim must be 64 or 128 and dtype ATTN_F16 or ATTN_BF16";
+    case ATTN_ERR_SHAPE: return "ATTN_ERR_SHAPE: invalid sizes (need B,Hq,Hkv,Lq,Lk >= 1, Hq % Hkv == 0, num_splits >= 0, window >= 0, finite scale, finite softcap >= 0)";
+    case ATTN_ERR_UNSUPPORTED: return "ATTN_ERR_UNSUPPORTED: head dim must be 64 or 128 and dtype ATTN_F16 or ATTN_BF16; softcap and window need the causal mask, softcap excludes ALiBi";
     case ATTN_ERR_WORKSPACE: return "ATTN_ERR_WORKSPACE: decode workspace too small";
     case ATTN_ERR_HIP: return "ATTN_ERR_HIP: a HIP launch failed (see attn_last_hip_error)";
     default: return "unknown attn_status";
@@ -75,15 +85,16 @@ const char* attn_status_string(int status) {
 
 int attn_last_hip_error(void) { return g_last_hip_error; }
 
-int attn_fwd(const void* Q, const void* K, const void* V, void* O,
-             int B, int Hq, int Hkv, int Lq, int Lk, int D,
-             int causal, float scale, const float* alibi_slopes, float softcap,
-             attn_dtype dtype, hipStream_t stream) {
+int attn_fwd_mod(const void* Q, const void* K, const void* V, void* O,
+                 int B, int Hq, int Hkv, int Lq, int Lk, int D,
+                 int causal, float scale, const float* alibi_slopes, float softcap, int window,
+                 attn_dtype dtype, hipStream_t stream) {
   if (!Q || !K || !V || !O) return ATTN_ERR_NULL;
   if (!shape_ok(B, Hq, Hkv, Lq, Lk) || !std::isfinite(scale)) return ATTN_ERR_SHAPE;
-  if (!std::isfinite(softcap) || softcap < 0.f) return ATTN_ERR_SHAPE;
+  if (!std::isfinite(softcap) || softcap < 0.f || window < 0) return ATTN_ERR_SHAPE;
   if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
   if (softcap > 0.f && (!causal || alibi_slopes)) return ATTN_ERR_UNSUPPORTED;
+  if (window > 0 && !causal) return ATTN_ERR_UNSUPPORTED;
   if (!sizes_fit(B, Hq, Hkv, Lq, Lk, D)) return ATTN_ERR_SHAPE;
   const int bm = attn::prefill_block_rows();
   const int64_t nqb = ((int64_t)Lq + bm - 1) / bm;
@@ -98,6 +109,7 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
   p.bf16 = dtype == ATTN_BF16;
   p.cap_k2 = softcap > 0.f ? 2.f / softcap : 0.f;
   p.cap_cl = softcap > 0.f ? softcap * kLog2e : 0.f;
+  p.window = window;
   if (alibi_slopes || softcap > 0.f) {
     p.c = scale * kLog2e;
     p.qsign = 0;
@@ -113,6 +125,13 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
   return e == hipSuccess ? ATTN_OK : hip_fail(e);
 }
 
+int attn_fwd(const void* Q, const void* K, const void* V, void* O,
+             int B, int Hq, int Hkv, int Lq, int Lk, int D,
+             int causal, float scale, const float* alibi_slopes,
+             attn_dtype dtype, hipStream_t stream) {
+  return attn_fwd_mod(Q, K, V, O, B, Hq, Hkv, Lq, Lk, D, causal, scale, alibi_slopes, 0.f, 0, dtype, stream);
+}
+
 int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D) {
   if (!shape_ok(B, Hq, Hkv, 1, Lk) || (D != 64 && D != 128)) return 0;
   const int group = Hq / Hkv;
@@ -125,7 +144,7 @@ int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D) {
     if (s < 1) s = 1;
     return (int)s;
   }
-  const int64_t groups = Hq / Hkv / gqa_heads_per_block(Hq / Hkv);
+  const int64_t groups = Hq / Hkv / decode_heads_per_block(Hq / Hkv);
   const int64_t units = (int64_t)B * Hkv * groups;
   int64_t s = (kTargetBlocks + units - 1) / units;
   const int64_t smax = ((int64_t)Lk + kMinChunk - 1) / kMinChunk;
@@ -141,7 +160,7 @@ size_t attn_decode_workspace_bytes(int B, int Hq, int D, int num_splits) {
   return (bytes + 255) & ~(size_t)255;
 }
 
-int attn_decode(const void* Q, const void* K, const void* V, void* O,
+int attn_decode_mod(const void* Q, const void* K, const void* V, void* O,
                 int B, int Hq, int Hkv, int Lk, int D,
                 float scale, const float* alibi_slopes, float softcap, int num_splits,
                 void* workspace, size_t workspace_bytes,
@@ -153,7 +172,7 @@ int attn_decode(const void* Q, const void* K, const void* V, void* O,
   if (!sizes_fit(B, Hq, Hkv, 1, Lk, D)) return ATTN_ERR_SHAPE;
   const int S = num_splits ? num_splits : attn_decode_num_splits(B, Hq, Hkv, Lk, D);
   const int group = Hq / Hkv;
-  const int64_t nblocks = (int64_t)S * (group / gqa_heads_per_block(group)) * Hkv * B;
+  const int64_t nblocks = (int64_t)S * (group / decode_heads_per_block(group)) * Hkv * B;
   if (nblocks > kMaxGrid || (int64_t)B * Hq > kMaxGrid) return ATTN_ERR_SHAPE;
   const size_t need = attn_decode_workspace_bytes(B, Hq, D, S);
   if (workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 15)) return ATTN_ERR_WORKSPACE;
@@ -175,6 +194,42 @@ int attn_decode(const void* Q, const void* K, const void* V, void* O,
   p.cap_cl = softcap > 0.f ? softcap * kLog2e : 0.f;
   hipError_t e = attn::launch_decode(p, stream);
   return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
+int attn_decode(const void* Q, const void* K, const void* V, void* O,
+                int B, int Hq, int Hkv, int Lk, int D,
+                float scale, const float* alibi_slopes, int num_splits,
+                void* workspace, size_t workspace_bytes,
+                attn_dtype dtype, hipStream_t stream) {
+  return attn_decode_mod(Q, K, V, O, B, Hq, Hkv, Lk, D, scale, alibi_slopes, 0.f, num_splits, workspace,
+                         workspace_bytes, dtype, stream);
+}
+
+int attn_fwd_kernels(int D, attn_dtype dtype, int causal, int alibi, float softcap, int window,
+                     char* buf, size_t len) {
+  if (!std::isfinite(softcap) || softcap < 0.f || window < 0) return ATTN_ERR_SHAPE;
+  if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
+  if ((softcap > 0.f && (!causal || alibi)) || (window > 0 && !causal)) return ATTN_ERR_UNSUPPORTED;
+  const attn::PrefillFlags f = attn::prefill_flags(causal != 0, alibi != 0, softcap > 0.f, window > 0);
+  char s[96];
+  std::snprintf(s, sizeof s, "prefill_kernel<%d,%s,%d,%d,%d,%d>", D, dtype_name(dtype), (int)f.causal, (int)f.alibi,
+                (int)f.cap, (int)f.win);
+  return put(buf, len, s);
+}
+
+int attn_decode_kernels(int Hq, int Hkv, int D, attn_dtype dtype, int alibi, float softcap, char* buf, size_t len) {
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || !std::isfinite(softcap) || softcap < 0.f) return ATTN_ERR_SHAPE;
+  if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
+  const int gh = attn::decode_split_heads(Hq / Hkv);
+  const int a = alibi ? 1 : 0, c = softcap > 0.f ? 1 : 0;
+  char s[160];
+  if (gh == 0)
+    std::snprintf(s, sizeof s, "decode_mfma_kernel<%d,%s,%d,%d>;decode_combine_kernel<%d,%s>", D, dtype_name(dtype), a,
+                  c, D, dtype_name(dtype));
+  else
+    std::snprintf(s, sizeof s, "decode_split_kernel<%d,%s,%d,%d,%d>;decode_combine_kernel<%d,%s>", D,
+                  dtype_name(dtype), gh, a, c, D, dtype_name(dtype));
+  return put(buf, len, s);
 }
 
 }  // extern "C"

@@ -280,7 +280,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
   }
   auto copy_tile = [&](int t, int bf) __attribute__((always_inline)) {
     const int k0 = kw0 + TN * t;
-    const int left = max(kw1 - k0, 0) * D * (int)sizeof(T);
+    const int left = min(max(kw1 - k0, 0), TN) * D * (int)sizeof(T);
 #pragma unroll
     for (int kv = 0; kv < 2; ++kv) {
       const uint64_t a = reinterpret_cast<uint64_t>((kv == 0 ? kbase : vbase) + (size_t)k0 * D);
@@ -543,11 +543,13 @@ hipError_t launch_mfma(const DecodeParams& p, hipStream_t stream) {
 // the vector kernel, whose lane groups stream key rows with nothing wasted.
 template <int D, typename T>
 hipError_t launch_g(const DecodeParams& p, hipStream_t stream) {
-  if (p.group >= 2 && p.group <= 32) return launch_mfma<D, T>(p, stream);
-  if (p.group % 8 == 0) return launch_split<D, T, 8>(p, stream);
-  if (p.group % 4 == 0) return launch_split<D, T, 4>(p, stream);
-  if (p.group % 2 == 0) return launch_split<D, T, 2>(p, stream);
-  return launch_split<D, T, 1>(p, stream);
+  switch (decode_split_heads(p.group)) {
+    case 0: return launch_mfma<D, T>(p, stream);
+    case 8: return launch_split<D, T, 8>(p, stream);
+    case 4: return launch_split<D, T, 4>(p, stream);
+    case 2: return launch_split<D, T, 2>(p, stream);
+    default: return launch_split<D, T, 1>(p, stream);
+  }
 }
 
 }  // namespace

@@ -20,6 +20,7 @@ struct PrefillParams {
   unsigned qsign;       // 0x80008000 to negate Q (negative scale, no ALiBi or SoftCap), else 0
   float cap_k2;         // SoftCap: 2 / cap
   float cap_cl;         // SoftCap: cap * log2(e), or 0 for no cap
+  int window;           // sliding window (keys per row, causal only), 0 for none
   int nqb;              // query blocks per head
   int nheads;           // B * Hq, set by the launcher
   int nitems;           // nqb * nheads, set by the launcher
@@ -45,6 +46,27 @@ struct DecodeParams {
   float cap_k2;         // SoftCap: 2 / cap
   float cap_cl;         // SoftCap: cap * log2(e), or 0 for no cap
 };
+
+// Template flags of the prefill kernel that a call launches.  SoftCap and the
+// sliding window are built for the causal mask (the entry point rejects the
+// other combinations), SoftCap without ALiBi.
+struct PrefillFlags {
+  bool causal, alibi, cap, win;
+};
+inline PrefillFlags prefill_flags(bool causal, bool alibi, bool cap, bool win) {
+  return {causal || cap || win, alibi && !cap, cap, win};
+}
+
+// Decode kernel for a GQA group of `group` query heads per KV head: 0 for the
+// grouped matrix-unit kernel (2..32 heads), else the heads per workgroup of
+// the vector split kernel (the largest of 8, 4, 2, 1 dividing the group).
+inline int decode_split_heads(int group) {
+  if (group >= 2 && group <= 32) return 0;
+  if (group % 8 == 0) return 8;
+  if (group % 4 == 0) return 4;
+  if (group % 2 == 0) return 2;
+  return 1;
+}
 
 int prefill_block_rows();
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);

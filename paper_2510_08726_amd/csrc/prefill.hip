@@ -260,7 +260,7 @@ struct SoftPlan {
   }
 };
 
-template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP>
+template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP, bool WIN>
 struct Prefill {
   // Scores are prepared in log2 units (the scale folded in) whenever a bias
   // or the cap has to act on the scaled value.
@@ -313,15 +313,16 @@ struct Prefill {
     float sl2;    // ALiBi slope * log2(e)
     float abase;  // ALiBi bias of key j0 + 4 hh relative to the wave's first row
     int lim;      // last visible key offset (key - j0 - 4 hh) of this lane's row
+    int llo;      // first visible key offset of this lane's row (sliding window)
     float t;      // this lane's maximum score of the tile
   };
 
   // HBM -> LDS copy of 1 KB block `blk` of key/value tile t (rows t BN ..
   // t BN + BN - 1) of one head (base) into the LDS slot at byte address
   // `slot`; dof is the lane's byte offset within the tile.  The buffer range
-  // ends at row `rows` (the workgroup's last staged row), so rows past it
-  // read as zero, and a tile past it (or a negative one) moves no data at
-  // all.  The tile offset lives in the (scalar) buffer base, so the lane
+  // ends at row `rows` (the workgroup's last staged row) or at the tile's
+  // end, whichever comes first, so rows past it read as zero, and a tile
+  // past it (or a negative one) has an empty range and writes zeros.  The tile offset lives in the (scalar) buffer base, so the lane
   // offset is the same register for every tile.  Issued as inline assembly:
   // the compiler then adds no waits of its own for the LDS writes; the kernel
   // waits for them explicitly before its barriers.
@@ -332,7 +333,7 @@ struct Prefill {
     // compiler computes the 64-bit address with vector instructions.
     const u32x4 rsrc = {(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
                         (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
-                        (uint32_t)__builtin_amdgcn_readfirstlane(left * D * (int)sizeof(T)), 0x00020000u};
+                        (uint32_t)__builtin_amdgcn_readfirstlane(min(left, BN) * D * (int)sizeof(T)), 0x00020000u};
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  : : "s"(slot + (uint32_t)(blk * 1024)), "v"(dof), "s"(rsrc) : "memory", "m0");
   }
@@ -413,7 +414,7 @@ struct Prefill {
           sc[r] = __builtin_fmaf(sc[r], ta.c, b[r - r0]);
         }
         if constexpr (MASKED) {
-          if (kconst(r) > ta.lim) sc[r] = kNegInf;
+          if (kconst(r) > ta.lim || (WIN && kconst(r) < ta.llo)) sc[r] = kNegInf;
         }
         float x = sc[r];
         pin(x);
@@ -564,9 +565,9 @@ struct Prefill {
 // registers: the 102 AGPRs named by the inline assembly and at most 152
 // VGPRs.  (By itself the compiler would halve the file once AGPRs are used;
 // the build sets the kernels' AGPR allocation to 104 in the device IR.)
-template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP>
+template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP, bool WIN>
 __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(152))) void prefill_kernel(PrefillParams p) {
-  typedef Prefill<D, T, CAUSAL, ALIBI, CAP> PF;
+  typedef Prefill<D, T, CAUSAL, ALIBI, CAP, WIN> PF;
   constexpr bool REV = ALIBI;
   typedef typename PF::State State;
   typedef typename PF::Scores Scores;
@@ -635,12 +636,15 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
   const int Lq = p.Lq, Lk = p.Lk;
   const int off = Lk - Lq;
 
-  // One work item: its query block and head, and the key tiles [0, nt) that
-  // the workgroup stages, [0, n_w) that this wave computes and [0, fm_w) that
-  // no row of the wave masks.
+  // One work item: its query block and head, the key tiles [t0, t1) that the
+  // workgroup stages (iteration j handles tile(j), j = 0 .. t1 - t0 - 1),
+  // the iterations [f0, f1] in which this wave sees keys and [w0, w1) in
+  // which no row of the wave masks any key of the tile.  rows: the staged
+  // key rows end there (rows past it read as zero).
   struct Item {
-    int qb, head, kvh, hq, iw, nt, n_w, fm_w, rows;
+    int qb, head, kvh, hq, iw, t0, t1, f0, f1, w0, w1, rows;
   };
+  const int W = WIN ? p.window : 0;   // sliding window (keys per row)
   auto item_at = [&](int round, Item& it) __attribute__((always_inline)) {
     const int sl = round * Pl + ((round & 1) ? Pl - 1 - c : c);
     if (sl >= s1 - s0) return false;
@@ -652,18 +656,32 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
     it.hq = it.head % p.Hq;
     const int i0 = it.qb * bm;
     it.iw = i0 + BMW * (wave / hg);
-    int kend = Lk, kend_w = Lk;
-    if (CAUSAL) {
-      kend = min(Lk, min(i0 + bm, Lq) + off);
-      kend_w = min(Lk, min(it.iw + BMW, Lq) + off);
+    // Row i sees keys [lo(i), hi(i)): hi(i) = i + off + 1 with the causal
+    // mask, lo(i) = i + off + 1 - W with the window (clamped to [0, Lk]).
+    auto hi = [&](int i) { return CAUSAL ? min(Lk, max(0, i + off + 1)) : Lk; };
+    auto lo = [&](int i) { return WIN ? min(Lk, max(0, i + off + 1 - W)) : 0; };
+    const int ilast = min(i0 + bm, Lq) - 1;               // the item's last row
+    const int klo = lo(i0), khi = hi(ilast);
+    it.t0 = klo / BN;
+    it.t1 = khi > klo ? (khi + BN - 1) / BN : it.t0;
+    it.rows = min(Lk, it.t1 * BN);
+    // This wave's rows [iw, wlast]: visible tiles [a, b), whole tiles
+    // [wl, wh) (every row sees every key of the tile).
+    const int wlast = min(it.iw + BMW, Lq) - 1;
+    int a = 0, b = 0, wl = 0, wh = 0;
+    if (it.iw < Lq && hi(wlast) > lo(it.iw)) {
+      a = lo(it.iw) / BN;
+      b = (hi(wlast) + BN - 1) / BN;
+      wl = (lo(wlast) + BN - 1) / BN;
+      wh = hi(it.iw) / BN;
     }
-    if (it.iw >= Lq) kend_w = 0;
-    it.nt = kend > 0 ? (kend + BN - 1) / BN : 0;
-    it.n_w = kend_w > 0 ? (kend_w + BN - 1) / BN : 0;
-    int fm = Lk / BN;
-    if (CAUSAL) fm = min(fm, max(0, (it.iw + off + 1) / BN));
-    it.fm_w = min(fm, it.n_w);
-    it.rows = min(Lk, it.nt * BN);
+    if (REV) {
+      it.f0 = it.t1 - b;  it.f1 = it.t1 - 1 - a;
+      it.w0 = it.t1 - wh; it.w1 = it.t1 - wl;
+    } else {
+      it.f0 = a - it.t0;  it.f1 = b - 1 - it.t0;
+      it.w0 = wl - it.t0; it.w1 = wh - it.t0;
+    }
     return true;
   };
   // Iteration j handles key tile tile(j).  With ALiBi the tiles are visited
@@ -671,7 +689,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
   // first tile holds the largest bias of each row and the running maximum
   // rarely grows afterwards (each growth beyond the lazy threshold costs a
   // rescale of O^T).  Otherwise the keys run forward.
-  auto tile_of = [&](const Item& it, int j) __attribute__((always_inline)) { return REV ? it.nt - 1 - j : j; };
+  auto tile_of = [&](const Item& it, int j) __attribute__((always_inline)) { return REV ? it.t1 - 1 - j : it.t0 + j; };
 
   Addr ad;
   PF::make_addr(ad, lane);
@@ -729,7 +747,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
   stage_q(cur);
 
   for (int round = 0;; ++round) {
-    const int nt = cur.nt, n_w = cur.n_w, fm_w = cur.fm_w;
+    const int nt = cur.t1 - cur.t0;   // iterations with a tile
     const int iw = cur.iw;
     const int row = iw + n;           // this lane's query row
     const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)cur.kvh * Lk * D;
@@ -794,10 +812,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
       int l = Lk - 1 - j0 - 4 * hh;
       if (CAUSAL) l = min(l, row + off - j0 - 4 * hh);
       ta.lim = l;
+      if (WIN) ta.llo = row + off + 1 - W - j0 - 4 * hh;
     };
     // The first iteration with a softmax: O^T and l are still zero there, so
     // its rescale is skipped.
-    const int jfirst = REV ? nt - n_w : 0;
+    const int jfirst = cur.f0;
     Scores sc[2];
     Probs pr[2];
     typename PF::template Ring<true> fk;
@@ -849,27 +868,46 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
     constexpr int FIRST_WHOLE = 1 + 2, FIRST_MASKED = 1 + 4;
     constexpr int WHOLE = 1 + 2 + 8, MASKED = 1 + 4 + 8, IDLE = 0;
     const std::integral_constant<int, IDLE> idle;
-    if (n_w == 0) {
+    const int f0 = cur.f0, f1 = cur.f1;
+    if (f1 < f0) {
       phase(iteration, -1, nt + 1, idle);
-    } else if constexpr (REV) {
-      // Visible tiles n_w - 1 .. 0 at iterations a .. nt - 1, masked ones first.
-      const int a = nt - n_w;
-      phase(iteration, -1, a - 1, idle);
-      phase(iteration, a - 1, a, std::integral_constant<int, PRO>{});
-      if (n_w > fm_w) phase(iteration, a, a + 1, std::integral_constant<int, FIRST_MASKED>{});
-      else phase(iteration, a, a + 1, std::integral_constant<int, FIRST_WHOLE>{});
-      phase(iteration, a + 1, nt - fm_w, std::integral_constant<int, MASKED>{});
-      phase(iteration, max(nt - fm_w, a + 1), nt, std::integral_constant<int, WHOLE>{});
+    } else if constexpr (!WIN && !REV) {
+      // Keys run forward from tile 0, which every wave sees (f0 = 0, w0 <= 0):
+      // the whole tiles come first, the masked ones (the causal diagonal, the
+      // ragged end) last.
+      iteration(-1, std::integral_constant<int, PRO>{}, std::integral_constant<int, kUnroll - 1>{});
+      if (cur.w1 > 0) iteration(0, std::integral_constant<int, FIRST_WHOLE>{}, std::integral_constant<int, 0>{});
+      else iteration(0, std::integral_constant<int, FIRST_MASKED>{}, std::integral_constant<int, 0>{});
+      phase(iteration, 1, cur.w1, std::integral_constant<int, WHOLE>{});
+      phase(iteration, max(cur.w1, 1), f1 + 1, std::integral_constant<int, MASKED>{});
+      phase(iteration, f1 + 1, f1 + 2, std::integral_constant<int, EPI>{});
+      phase(iteration, f1 + 2, nt + 1, idle);
+    } else if constexpr (!WIN) {
+      // Keys run from the last tile to tile 0, which every wave sees last
+      // (f1 = nt - 1, w1 = nt): the masked tiles come first.
+      phase(iteration, -1, f0 - 1, idle);
+      phase(iteration, f0 - 1, f0, std::integral_constant<int, PRO>{});
+      if (f0 >= cur.w0) phase(iteration, f0, f0 + 1, std::integral_constant<int, FIRST_WHOLE>{});
+      else phase(iteration, f0, f0 + 1, std::integral_constant<int, FIRST_MASKED>{});
+      phase(iteration, f0 + 1, cur.w0, std::integral_constant<int, MASKED>{});
+      phase(iteration, max(cur.w0, f0 + 1), nt, std::integral_constant<int, WHOLE>{});
       phase(iteration, nt, nt + 1, std::integral_constant<int, EPI>{});
     } else {
-      // Visible tiles 0 .. n_w - 1 at iterations 0 .. n_w - 1, masked ones last.
-      iteration(-1, std::integral_constant<int, PRO>{}, std::integral_constant<int, kUnroll - 1>{});
-      if (fm_w > 0) iteration(0, std::integral_constant<int, FIRST_WHOLE>{}, std::integral_constant<int, 0>{});
-      else iteration(0, std::integral_constant<int, FIRST_MASKED>{}, std::integral_constant<int, 0>{});
-      phase(iteration, 1, fm_w, std::integral_constant<int, WHOLE>{});
-      phase(iteration, max(fm_w, 1), n_w, std::integral_constant<int, MASKED>{});
-      phase(iteration, n_w, n_w + 1, std::integral_constant<int, EPI>{});
-      phase(iteration, n_w + 1, nt + 1, idle);
+      // Visible iterations f0 .. f1: the first one (no P.V yet), then the
+      // masked ones before the whole ones (the window's lower edge, or with
+      // ALiBi the causal diagonal), the whole ones, the masked ones after
+      // them (the causal diagonal, or with ALiBi the window's edge).
+      const int ws = min(max(cur.w0, f0 + 1), f1 + 1);
+      const int we = min(max(cur.w1, ws), f1 + 1);
+      phase(iteration, -1, f0 - 1, idle);
+      phase(iteration, f0 - 1, f0, std::integral_constant<int, PRO>{});
+      if (cur.w0 <= f0 && f0 < cur.w1) phase(iteration, f0, f0 + 1, std::integral_constant<int, FIRST_WHOLE>{});
+      else phase(iteration, f0, f0 + 1, std::integral_constant<int, FIRST_MASKED>{});
+      phase(iteration, f0 + 1, ws, std::integral_constant<int, MASKED>{});
+      phase(iteration, ws, we, std::integral_constant<int, WHOLE>{});
+      phase(iteration, we, f1 + 1, std::integral_constant<int, MASKED>{});
+      phase(iteration, f1 + 1, f1 + 2, std::integral_constant<int, EPI>{});
+      phase(iteration, f1 + 2, nt + 1, idle);
     }
     // The scores of the last iterations are dead, but are kept live past
     // the padding so that their registers are not reused while the MFMAs
@@ -941,7 +979,7 @@ int compute_units() {
   return n;
 }
 
-template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP>
+template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP, bool WIN = false>
 hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
   PrefillParams q = p;
   // Query heads per workgroup: the largest power of two (up to the wave
@@ -955,19 +993,20 @@ hipError_t launch_t(const PrefillParams& p, hipStream_t stream) {
   if (q.nitems == 0) return hipSuccess;
   const int grid = std::min(q.nitems, kWgPerCu * compute_units());
   q.nxcd = grid % kXcds == 0 ? kXcds : 1;
-  hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI, CAP>), dim3(grid), dim3(kThreads), 0, stream, q);
+  hipLaunchKernelGGL((prefill_kernel<D, T, CAUSAL, ALIBI, CAP, WIN>), dim3(grid), dim3(kThreads), 0, stream, q);
   return hipGetLastError();
 }
 
 template <int D, typename T>
 hipError_t launch_d(const PrefillParams& p, hipStream_t s) {
-  // SoftCap is built for the causal mask without ALiBi (the SoftCap operator);
-  // the entry point rejects the other combinations.
-  if (p.cap_cl != 0.f) return launch_t<D, T, true, false, true>(p, s);
-  if (p.causal) {
-    return p.slopes ? launch_t<D, T, true, true, false>(p, s) : launch_t<D, T, true, false, false>(p, s);
+  const PrefillFlags f = prefill_flags(p.causal != 0, p.slopes != nullptr, p.cap_cl != 0.f, p.window > 0);
+  if (f.win) {
+    if (f.cap) return launch_t<D, T, true, false, true, true>(p, s);
+    return f.alibi ? launch_t<D, T, true, true, false, true>(p, s) : launch_t<D, T, true, false, false, true>(p, s);
   }
-  return p.slopes ? launch_t<D, T, false, true, false>(p, s) : launch_t<D, T, false, false, false>(p, s);
+  if (f.cap) return launch_t<D, T, true, false, true>(p, s);
+  if (f.causal) return f.alibi ? launch_t<D, T, true, true, false>(p, s) : launch_t<D, T, true, false, false>(p, s);
+  return f.alibi ? launch_t<D, T, false, true, false>(p, s) : launch_t<D, T, false, false, false>(p, s);
 }
 
 }  // namespace

@@ -36,6 +36,7 @@ class Workload:
     num_splits: int = 0
     scale: float = field(default=None)
     softcap: float = 0.0      # SoftCap cap (0: none)
+    window: int = 0           # causal sliding window in keys (0: none)
 
     @property
     def sm_scale(self):
@@ -45,7 +46,9 @@ class Workload:
 # The six shapes the headline metric is quoted on, then ALiBi decode (the MHA
 # decode shape with the ALiBi bias) and SoftCap decode (Gemma 2 27B's
 # attention: 32 query heads on 16 KV heads of dim 128, logits capped at 50), and
-# SoftCap causal prefill with the same heads.
+# SoftCap causal prefill with the same heads, and the Window operator with
+# Gemma 2 27B's local-attention layers: the same heads, a causal sliding window
+# of 4096 keys, L = 8192.
 # Prefill: Lq == Lk.  Decode: one query token (Lq = 1) against a KV cache of
 # Lk keys.
 WORKLOADS = {
@@ -68,6 +71,8 @@ WORKLOADS = {
                                decode=True, seed=8, softcap=50.0),
     "softcap_causal_prefill": Workload("softcap_causal_prefill", 2, 32, 16, 4096, 4096,
                                        128, "f16", causal=True, seed=9, softcap=50.0),
+    "window_causal_prefill": Workload("window_causal_prefill", 2, 32, 16, 8192, 8192,
+                                      128, "f16", causal=True, seed=10, window=4096),
 }
 
 
@@ -112,17 +117,20 @@ def random_tensors(shapes, dtype, seed, device="cpu"):
     return res
 
 
-def prefill_flops(B, Hq, Lq, Lk, D, causal):
+def prefill_flops(B, Hq, Lq, Lk, D, causal, window=0):
     """Algorithmic FLOPs: 4 * D per visible (query, key) pair, over all heads.
 
     Two contractions (Q.K^T and P.V), 2 flops per multiply-add; softmax work
-    is not counted.  Causal visibility is bottom-right aligned.
+    is not counted.  Causal visibility is bottom-right aligned; a window of W
+    keys leaves row i the keys i_abs - W < j <= i_abs.
     """
     if causal:
         off = Lk - Lq
         visible = 0
         for i in range(Lq):
-            visible += max(0, min(Lk, i + off + 1))
+            hi = min(Lk, i + off + 1)
+            lo = max(0, i + off + 1 - window) if window else 0
+            visible += max(0, hi - lo)
     else:
         visible = Lq * Lk
     return 4 * D * visible * B * Hq

@@ -42,15 +42,17 @@ def assert_close(gpu_out, ref, what=""):
     return e
 
 
-def run_fwd(q, k, v, *, scale, causal=False, slopes=None, softcap=None):
+def run_fwd(q, k, v, *, scale, causal=False, slopes=None, softcap=None, window=None):
     dev = torch.device("cuda")
     o = pa.attn_fwd(q.to(dev), k.to(dev), v.to(dev), causal=causal, scale=scale,
-                    alibi_slopes=None if slopes is None else slopes.to(dev), softcap=softcap)
+                    alibi_slopes=None if slopes is None else slopes.to(dev), softcap=softcap,
+                    window=window)
     torch.cuda.synchronize()
     return o
 
 
-def oracle_fwd(q, k, v, *, scale, causal=False, slopes=None, softcap=None, rows=None, heads=None):
+def oracle_fwd(q, k, v, *, scale, causal=False, slopes=None, softcap=None, window=None, rows=None,
+               heads=None):
     sl = None if slopes is None else host64(slopes)
     return oracle.attention(host32(q), host32(k), host32(v), scale=scale, causal=causal,
-                            alibi_slopes=sl, softcap=softcap, rows=rows, heads=heads)
+                            alibi_slopes=sl, softcap=softcap, window=window, rows=rows, heads=heads)

@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert {"attn_fwd", "attn_decode", "attn_decode_workspace_bytes",
+    assert {"attn_fwd", "attn_fwd_mod", "attn_decode", "attn_decode_mod", "attn_decode_workspace_bytes",
             "attn_decode_num_splits", "attn_status_string", "attn_last_hip_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
@@ -49,8 +49,12 @@ def test_status_strings(lib):
 
 
 def fwd(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=1, Hq=2, Hkv=2, Lq=8, Lk=8, D=64, causal=0,
-        scale=0.125, slopes=NULL, cap=0.0, dtype=0):
-    return lib.attn_fwd(q, k, v, o, B, Hq, Hkv, Lq, Lk, D, causal, scale, slopes, cap, dtype, NULL)
+        scale=0.125, slopes=NULL, cap=0.0, window=0, dtype=0):
+    rc = lib.attn_fwd_mod(q, k, v, o, B, Hq, Hkv, Lq, Lk, D, causal, scale, slopes, cap, window, dtype, NULL)
+    if cap == 0.0 and window == 0:
+        # the boundary's own signature answers the same way
+        assert lib.attn_fwd(q, k, v, o, B, Hq, Hkv, Lq, Lk, D, causal, scale, slopes, dtype, NULL) == rc
+    return rc
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -64,6 +68,10 @@ def fwd(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=1, Hq=2, Hkv=2, Lq=8, Lk=8, D=64,
     (dict(causal=1, cap=-2.0), pa.ATTN_ERR_SHAPE), (dict(causal=1, cap=float("nan")), pa.ATTN_ERR_SHAPE),
     (dict(cap=30.0), pa.ATTN_ERR_UNSUPPORTED),                       # SoftCap without the causal mask
     (dict(causal=1, cap=30.0, slopes=FAKE), pa.ATTN_ERR_UNSUPPORTED),  # SoftCap with ALiBi
+    (dict(causal=1, window=-1), pa.ATTN_ERR_SHAPE),
+    (dict(window=16), pa.ATTN_ERR_UNSUPPORTED),                      # window without the causal mask
+    (dict(causal=1, window=4, D=96), pa.ATTN_ERR_UNSUPPORTED),
+    (dict(causal=1, window=4, q=NULL), pa.ATTN_ERR_NULL),
     (dict(dtype=2), pa.ATTN_ERR_UNSUPPORTED),
     (dict(B=1 << 20, Hq=1 << 10, Hkv=1 << 10, Lq=1 << 20, Lk=1 << 20), pa.ATTN_ERR_SHAPE),
 ])
@@ -73,7 +81,10 @@ def test_fwd_rejects_bad_arguments(lib, kw, code):
 
 def dec(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=2, Hq=8, Hkv=2, Lk=100, D=128, scale=0.1,
         slopes=NULL, cap=0.0, S=4, ws=FAKE, ws_bytes=1 << 30, dtype=0):
-    return lib.attn_decode(q, k, v, o, B, Hq, Hkv, Lk, D, scale, slopes, cap, S, ws, ws_bytes, dtype, NULL)
+    rc = lib.attn_decode_mod(q, k, v, o, B, Hq, Hkv, Lk, D, scale, slopes, cap, S, ws, ws_bytes, dtype, NULL)
+    if cap == 0.0:
+        assert lib.attn_decode(q, k, v, o, B, Hq, Hkv, Lk, D, scale, slopes, S, ws, ws_bytes, dtype, NULL) == rc
+    return rc
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -130,3 +141,20 @@ def test_binding_rejects_cpu_tensors():
     q = torch.zeros(1, 1, 4, 64, dtype=torch.float16)
     with pytest.raises(ValueError):
         pa.attn_fwd(q, q, q)
+
+
+def test_boundary_signatures_match_the_scope_table():
+    """attn_fwd / attn_decode take exactly the boundary's arguments (no modifier
+    inserted between them); the modifiers live in the *_mod entry points."""
+    src = open(os.path.join(ROOT, "include", "attn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+
+    def params(name):
+        m = re.search(r"\b%s\s*\(([^)]*)\)\s*;" % name, src)
+        return [re.split(r"[\s*]+", p.strip())[-1] for p in m.group(1).split(",")]
+    assert params("attn_fwd") == ["Q", "K", "V", "O", "B", "Hq", "Hkv", "Lq", "Lk", "D", "causal", "scale",
+                                  "alibi_slopes", "dtype", "stream"]
+    assert params("attn_decode") == ["Q", "K", "V", "O", "B", "Hq", "Hkv", "Lk", "D", "scale", "alibi_slopes",
+                                     "num_splits", "workspace", "workspace_bytes", "dtype", "stream"]
+    assert params("attn_fwd_mod")[-4:] == ["softcap", "window", "dtype", "stream"]
+    assert params("attn_decode_mod")[10:13] == ["alibi_slopes", "softcap", "num_splits"]

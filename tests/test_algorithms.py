@@ -129,3 +129,13 @@ def test_split_k_with_softcap_equals_plain_definition(S, alibi):
     np.testing.assert_allclose(o, ref, atol=1e-12, rtol=0)
     plain = oracle.attention(q, k, v, scale=0.35, causal=True, alibi_slopes=sl)
     assert np.abs(ref - plain).max() > 1e-2          # the cap changes the result at these scores
+
+
+@pytest.mark.parametrize("W,block_n", [(1, 4), (7, 8), (40, 16)])
+def test_rolling_update_with_window_equals_plain_definition(W, block_n):
+    """Theorem 1 holds for any mask: the rolling update over the windowed scores."""
+    q, k, v = _rand((1, 2, 33, 8), 91), _rand((1, 2, 45, 8), 92), _rand((1, 2, 45, 8), 93)
+    ref = oracle.attention(q, k, v, scale=0.4, causal=True, window=W)
+    for hq in range(2):
+        got = rolling.rolling_update_attention(q, k, v, scale=0.4, causal=True, window=W, block_n=block_n, hq=hq)
+        np.testing.assert_allclose(got, ref[0, hq], atol=1e-12)

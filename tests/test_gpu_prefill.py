@@ -116,34 +116,78 @@ def test_prefill_is_deterministic():
 
 
 # ---------------------------------------------------------------------------
-# full-size workloads (the bench's launch configuration), sampled rows
+# full-size workloads (the bench's launch configuration)
 
 @functools.lru_cache(maxsize=1)
 def _workload_run(name):
     w = WORKLOADS[name]
     q, k, v, sl = make_inputs(w)
-    o = run_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl, softcap=w.softcap or None)
+    dev = torch.device("cuda")
+    # NaN-filled output: a row that no work item writes cannot pass.
+    o = torch.full(q.shape, float("nan"), dtype=q.dtype, device=dev)
+    pa.attn_fwd(q.to(dev), k.to(dev), v.to(dev), o, causal=w.causal, scale=w.sm_scale,
+                alibi_slopes=None if sl is None else sl.to(dev), softcap=w.softcap or None,
+                window=w.window or None)
+    torch.cuda.synchronize()
     return w, q, k, v, sl, o.cpu()
 
 
+def _wave_block_rows(L):
+    """The first and the last row of every 32-row wave block (every wave of
+    every work item of the persistent schedule), plus a few in between."""
+    rows = set()
+    for r0 in range(0, L, 32):
+        rows.update((r0, min(r0 + 31, L - 1)))
+    rows.update(range(L // 2 - 3, L // 2 + 3))
+    return sorted(rows)
+
+
 @pytest.mark.parametrize("name", ["tiny_noncausal", "causal_mha_prefill", "gqa_causal_prefill",
-                                  "alibi_causal_prefill", "softcap_causal_prefill"])
-def test_prefill_workload_sampled_rows(name):
+                                  "alibi_causal_prefill", "softcap_causal_prefill", "window_causal_prefill"])
+def test_prefill_workload_full_size(name):
+    """Every (batch, head).  The causal MHA workload (and the tiny one) is
+    compared on every row; the others on the first and last row of every
+    32-row wave block, so every wave of every work item is checked."""
     print(f"prefill workload {name}", flush=True)
     w, q, k, v, sl, o = _workload_run(name)
-    rng = np.random.Generator(np.random.PCG64(99))
-    L = w.Lq
-    rows = sorted(set([0, 1, 2, 31, 32, 63, 64, 127, 128, 129, L // 2, L - 65, L - 64, L - 2, L - 1]
-                      + list(rng.integers(0, L, 16))))
-    rows = [r for r in rows if 0 <= r < L]
-    heads = sorted(set([(0, 0), (w.B - 1, w.Hq - 1), (0, w.Hq // 2)]
-                       + [(int(rng.integers(w.B)), int(rng.integers(w.Hq))) for _ in range(3)]))
+    got = host32(o)
+    assert np.all(np.isfinite(got)), "every output row is written"
+    full = name in ("tiny_noncausal", "causal_mha_prefill")
+    rows = None if full else _wave_block_rows(w.Lq)
     ref = oracle_fwd(q, k, v, scale=w.sm_scale, causal=w.causal, slopes=sl, softcap=w.softcap or None,
-                     rows=rows, heads=heads)
-    got = host32(o)[:, :, rows]
-    sel_b = [b for b, _ in heads]
-    sel_h = [h for _, h in heads]
-    assert_close(got[sel_b, sel_h], ref[sel_b, sel_h], f"{name} sampled")
+                     window=w.window or None, rows=rows)
+    assert_close(got if full else got[:, :, rows], ref, f"{name} {'all rows' if full else 'wave-block rows'}")
+
+
+MULTI_ROUND_CASES = [  # B, Hq, Hkv, L_q, L_k, D, dtype, alibi, window: more work items than workgroups
+    (4, 64, 64, 600, 600, 64, "f16", False, None),     # 1280 items: 2-3 rounds per workgroup
+    (4, 64, 64, 600, 600, 64, "bf16", True, None),     # ALiBi: keys last to first
+    (2, 64, 8, 600, 600, 128, "f16", False, None),     # 8 query heads per KV head: 608 items
+    (3, 48, 48, 400, 650, 64, "f16", False, None),     # Lq < Lk
+    (3, 48, 48, 650, 400, 128, "bf16", False, None),   # Lq > Lk: rows and waves with no key
+    (4, 64, 32, 600, 600, 64, "f16", False, 90),       # sliding window, 2 heads per KV head
+]
+
+
+@pytest.mark.parametrize("case", MULTI_ROUND_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_prefill_multi_round_matches_oracle_everywhere(case):
+    """The persistent schedule's later rounds: the next item's staging before
+    the current output, the snake order, compared on every output element."""
+    B, Hq, Hkv, Lq, Lk, D, dt, alibi, win = case
+    print(f"multi-round prefill case {case}", flush=True)
+    q, k, v = random_tensors([(B, Hq, Lq, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], dt,
+                             seed=zlib.crc32(repr(case).encode()) % 1000)
+    sl = alibi_slopes(Hq) if alibi else None
+    dev = torch.device("cuda")
+    o = torch.full((B, Hq, Lq, D), float("nan"), dtype=q.dtype, device=dev)
+    pa.attn_fwd(q.to(dev), k.to(dev), v.to(dev), o, causal=True, scale=D ** -0.5,
+                alibi_slopes=None if sl is None else sl.to(dev), window=win)
+    torch.cuda.synchronize()
+    got = host32(o)
+    ref = oracle_fwd(q, k, v, scale=D ** -0.5, causal=True, slopes=sl, window=win)
+    assert_close(got, ref, f"multi-round {case}")
+    if Lq > Lk:
+        assert np.all(got[:, :, :Lq - Lk] == 0)
 
 
 SOFTCAP_CASES = [  # B, Hq, Hkv, Lq, Lk, D, dtype, cap, score gain
@@ -182,3 +226,48 @@ def test_prefill_softcap_last_row_equals_decode():
                         softcap=cap, num_splits=3)
     torch.cuda.synchronize()
     assert_close(o[:, :, -1:], host64(od.cpu()).astype(np.float64), "prefill last row vs decode")
+
+
+WINDOW_CASES = [  # B, Hq, Hkv, Lq, Lk, D, dtype, window, alibi, softcap
+    (1, 2, 2, 300, 300, 128, "f16", 1, False, None),        # one key per row: O = V[i]
+    (2, 4, 2, 333, 333, 64, "bf16", 45, False, None),       # band edges inside tiles, ragged tail
+    (1, 4, 4, 700, 700, 128, "f16", 100, False, None),      # several 128-row blocks, edges off the grid
+    (1, 2, 1, 257, 600, 128, "bf16", 64, False, None),      # Lq < Lk, band edge on the tile grid
+    (1, 2, 2, 400, 150, 64, "f16", 70, False, None),        # Lq > Lk: the first rows see no key
+    (1, 16, 2, 300, 300, 128, "bf16", 33, False, None),     # 8 query heads per KV head
+    (1, 4, 4, 520, 520, 64, "f16", 96, True, None),         # ALiBi: keys visited last to first
+    (1, 2, 2, 300, 777, 128, "bf16", 200, True, None),      # ALiBi, Lk > Lq
+    (1, 4, 2, 300, 300, 128, "f16", 57, False, 3.0),        # with SoftCap (Gemma 2 local layers)
+    (1, 2, 2, 129, 129, 64, "f16", 5000, False, None),      # window wider than every row: causal
+]
+
+
+@pytest.mark.parametrize("case", WINDOW_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_prefill_window_matches_oracle(case):
+    B, Hq, Hkv, Lq, Lk, D, dt, W, alibi, cap = case
+    print(f"window prefill case {case}", flush=True)
+    q, k, v = random_tensors([(B, Hq, Lq, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], dt,
+                             seed=zlib.crc32(repr(case).encode()) % 1000)
+    if cap:
+        q = (q.float() * 4).to(q.dtype)
+    sl = alibi_slopes(Hq) if alibi else None
+    scale = D ** -0.5
+    o = run_fwd(q, k, v, scale=scale, causal=True, slopes=sl, softcap=cap, window=W)
+    ref = oracle_fwd(q, k, v, scale=scale, causal=True, slopes=sl, softcap=cap, window=W)
+    assert_close(host32(o), ref, f"window prefill {case}")
+    if W == 1:
+        G = Hq // Hkv
+        off = Lk - Lq
+        vv = host32(v).repeat(G, axis=1)
+        rows = [i for i in range(Lq) if i + off >= 0]
+        np.testing.assert_array_equal(host32(o)[:, :, rows], vv[:, :, [i + off for i in rows]])
+
+
+def test_prefill_window_scale_zero_is_band_mean():
+    """scale = 0: every row averages V over its band (closed form)."""
+    B, H, L, D, W = 1, 2, 300, 64, 37
+    q, k, v = random_tensors([(B, H, L, D)] * 3, "f16", seed=66)
+    o = host32(run_fwd(q, k, v, scale=0.0, causal=True, window=W))
+    vv = host64(v)
+    ref = np.stack([vv[:, :, max(0, i - W + 1):i + 1].mean(axis=2) for i in range(L)], axis=2)
+    np.testing.assert_allclose(o, ref, atol=4e-3)

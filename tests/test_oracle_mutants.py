@@ -226,7 +226,8 @@ def test_mutant_softcap_missing_inner_division_is_caught():
 def _scores_in_order(bias_inside, mask_first):
     base = _ATT.scores
 
-    def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, b=0, hq=0, rows=None):
+    def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, window=None, b=0, hq=0,
+               rows=None):
         if not softcap:
             return base(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes, b=b, hq=hq, rows=rows)
         raw = base(q, k, scale=scale, causal=False, alibi_slopes=alibi_slopes if bias_inside else None,
@@ -257,3 +258,97 @@ def test_softcap_planted_order_helper_matches_oracle_when_correct():
     """The helper that builds the two order mutants is itself right when given the right order."""
     good = _patched("scores", _scores_in_order(bias_inside=False, mask_first=False))
     assert all(pin(good) for pin in SOFTCAP_PINS)
+
+
+# ---------------------------------------------------------------------------
+# sliding window: the band pins must reject an off-by-one edge, a band on
+# the wrong side of the diagonal and a window that is ignored
+
+def _window_one_pin(attn):
+    """W = 1: every row with a key at its own position returns that V row."""
+    q, k, v = _rand((1, 2, 9, 4), 41), _rand((1, 2, 12, 4), 42), _rand((1, 2, 12, 4), 43)
+    o = attn(q, k, v, scale=0.8, causal=True, window=1)
+    return all(np.allclose(o[0, h, i], v[0, h, i + 3], atol=1e-13) for h in range(2) for i in range(9))
+
+
+def _band_mean_pin(attn):
+    """scale = 0: row i averages V over keys max(0, i_abs - W + 1) .. i_abs."""
+    W = 4
+    q, k, v = _rand((1, 1, 7, 3), 44), _rand((1, 1, 10, 3), 45), _rand((1, 1, 10, 3), 46)
+    o = attn(q, k, v, scale=0.0, causal=True, window=W)
+    for i in range(7):
+        ia = i + 3
+        band = [v[0, 0, j] for j in range(max(0, ia - W + 1), ia + 1)]
+        if not np.allclose(o[0, 0, i], sum(band) / len(band), atol=1e-13):
+            return False
+    return True
+
+
+WINDOW_PINS = [_window_one_pin, _band_mean_pin]
+
+
+def _windowed(edge):
+    """Oracle with the band edge replaced: edge(j, i_abs, W) -> visible."""
+    base = _ATT.scores
+
+    def scores(q, k, *, scale, causal=False, alibi_slopes=None, softcap=None, window=None, b=0, hq=0,
+               rows=None):
+        s = base(q, k, scale=scale, causal=causal, alibi_slopes=alibi_slopes, softcap=softcap, b=b, hq=hq,
+                 rows=rows)
+        if not window:
+            return s
+        Lq, Lk = q.shape[2], k.shape[2]
+        i = (np.arange(Lq) if rows is None else np.asarray(rows))[:, None] + (Lk - Lq)
+        return np.where(edge(np.arange(Lk)[None, :], i, int(window)), s, -np.inf)
+    return _patched("scores", scores)
+
+
+def test_true_oracle_passes_every_window_pin():
+    for pin in WINDOW_PINS:
+        assert pin(oracle.attention), pin.__name__
+
+
+def test_window_helper_matches_oracle_when_correct():
+    good = _windowed(lambda j, i, W: j > i - W)
+    assert all(pin(good) for pin in WINDOW_PINS)
+
+
+def test_mutant_window_off_by_one_is_caught():
+    assert any(not pin(_windowed(lambda j, i, W: j >= i - W)) for pin in WINDOW_PINS)
+
+
+def test_mutant_window_on_the_wrong_side_is_caught():
+    assert any(not pin(_windowed(lambda j, i, W: j < i + W)) for pin in WINDOW_PINS)
+
+
+def test_mutant_window_ignored_is_caught():
+    assert any(not pin(_windowed(lambda j, i, W: np.ones_like(j - i, dtype=bool))) for pin in WINDOW_PINS)
+
+
+# ---------------------------------------------------------------------------
+# softmax_probs: a max taken over the wrong axis keeps row sums at 1 but not
+# the values, which the Lk = 2 logistic pin of the probabilities checks
+
+def _probs_logistic_pin(probs):
+    q, k = _rand((1, 1, 4, 5), 51), _rand((1, 1, 2, 5), 52)
+    p = probs(q, k, scale=0.6)
+    for i in range(4):
+        s = [0.6 * math.fsum(float(q[0, 0, i, d]) * float(k[0, 0, j, d]) for d in range(5)) for j in range(2)]
+        if not np.isclose(p[i, 0], 1.0 / (1.0 + math.exp(s[1] - s[0])), atol=1e-13, rtol=0):
+            return False
+    return True
+
+
+def test_true_softmax_probs_passes_logistic_pin():
+    assert _probs_logistic_pin(oracle.softmax_probs)
+
+
+def test_mutant_softmax_max_over_wrong_axis_is_caught():
+    def probs(q, k, **kw):
+        score = oracle.scores(q, k, **kw)
+        m = score.max(axis=0, keepdims=True)          # column max instead of row max
+        e = np.exp(score - m)
+        return e / e.sum(axis=1, keepdims=True)
+    p = probs(_rand((1, 1, 4, 5), 51), _rand((1, 1, 2, 5), 52), scale=0.6)
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-12)   # row sums do not notice
+    assert not _probs_logistic_pin(probs)

@@ -243,3 +243,100 @@ def test_softcap_bounds_the_weight_ratio():
         for i in range(9):
             row = p[i, :i + 30 - 9 + 1]
             assert np.all(row > 0) and row.max() / row.min() <= math.exp(2 * cap) * (1 + 1e-12)
+
+
+# ---------------------------------------------------------------------------
+# softmax_probs values (not only their row sums)
+
+def test_softmax_probs_two_keys_logistic():
+    """Lk = 2: P[i, 0] = 1 / (1 + e^(s1 - s0)), scores summed by hand."""
+    q, k = _rand((1, 2, 5, 7), 61), _rand((1, 1, 2, 7), 62)
+    for hq in range(2):
+        p = oracle.softmax_probs(q, k, scale=0.45, hq=hq)
+        for i in range(5):
+            s = [0.45 * math.fsum(q[0, hq, i, d] * k[0, 0, j, d] for d in range(7)) for j in range(2)]
+            w0 = 1.0 / (1.0 + math.exp(s[1] - s[0]))
+            assert abs(p[i, 0] - w0) <= 1e-13 and abs(p[i, 1] - (1.0 - w0)) <= 1e-13
+
+
+@pytest.mark.parametrize("Lq,Lk", [(6, 6), (4, 9)])
+def test_softmax_probs_causal_scale_zero_uniform(Lq, Lk):
+    """scale = 0, causal: row i spreads 1 / (i_abs + 1) over keys 0 .. i_abs."""
+    q, k = _rand((1, 1, Lq, 3), 63), _rand((1, 1, Lk, 3), 64)
+    p = oracle.softmax_probs(q, k, scale=0.0, causal=True)
+    for i in range(Lq):
+        ia = i + Lk - Lq
+        for j in range(Lk):
+            assert p[i, j] == (1.0 / (ia + 1) if j <= ia else 0.0) or abs(p[i, j] - 1.0 / (ia + 1)) < 1e-15
+
+
+# ---------------------------------------------------------------------------
+# sliding window (Window operator of Table tab:operators; causal band of W keys)
+
+@pytest.mark.parametrize("Lq,Lk", [(9, 9), (5, 13), (11, 7)])
+def test_window_covering_every_key_is_causal(Lq, Lk):
+    q, k, v = _rand((1, 2, Lq, 4), 71), _rand((1, 1, Lk, 4), 72), _rand((1, 1, Lk, 4), 73)
+    ref = oracle.attention(q, k, v, scale=0.7, causal=True)
+    for W in (Lk, Lk + 3, 10 ** 6):
+        np.testing.assert_array_equal(oracle.attention(q, k, v, scale=0.7, causal=True, window=W), ref)
+
+
+@pytest.mark.parametrize("Lq,Lk", [(8, 8), (5, 12), (10, 6)])
+def test_window_of_one_key_selects_its_value(Lq, Lk):
+    q, k, v = _rand((2, 2, Lq, 6), 74), _rand((2, 2, Lk, 6), 75), _rand((2, 2, Lk, 6), 76)
+    o = oracle.attention(q, k, v, scale=1.3, causal=True, window=1)
+    for i in range(Lq):
+        ia = i + Lk - Lq
+        if ia >= 0:
+            np.testing.assert_array_equal(o[:, :, i], v[:, :, ia])
+        else:
+            assert np.all(o[:, :, i] == 0)
+
+
+@pytest.mark.parametrize("W", [1, 2, 5, 30])
+def test_window_scale_zero_is_band_mean(W):
+    Lq, Lk = 12, 20
+    q, k, v = _rand((1, 1, Lq, 3), 77), _rand((1, 1, Lk, 3), 78), _rand((1, 1, Lk, 3), 79)
+    o = oracle.attention(q, k, v, scale=0.0, causal=True, window=W)
+    for i in range(Lq):
+        ia = i + Lk - Lq
+        band = [v[0, 0, j] for j in range(max(0, ia - W + 1), ia + 1)]
+        np.testing.assert_allclose(o[0, 0, i], sum(band) / len(band), atol=1e-14)
+
+
+def test_window_alibi_scale_zero_geometric_band():
+    H, L, W = 3, 15, 4
+    q, k, v = _rand((1, H, L, 2), 80), _rand((1, H, L, 2), 81), _rand((1, H, L, 2), 82)
+    sl = alibi_slopes(H).double().numpy()
+    o = oracle.attention(q, k, v, scale=0.0, causal=True, alibi_slopes=sl, window=W)
+    for h in range(H):
+        r = math.exp(-sl[h])
+        for i in range(L):
+            js = range(max(0, i - W + 1), i + 1)
+            w = np.array([r ** (i - j) for j in js])
+            ref = (w[:, None] * v[0, h, list(js)]).sum(0) / w.sum()
+            np.testing.assert_allclose(o[0, h, i], ref, atol=1e-13)
+
+
+@pytest.mark.parametrize("Lq,Lk,W,G", [(16, 16, 5, 1), (7, 19, 6, 2), (13, 9, 3, 4)])
+def test_window_matches_torch_sdpa_with_band_mask(Lq, Lk, W, G):
+    """Library special case: PyTorch float64 SDPA with an explicit band mask."""
+    Hkv = 2
+    q, k, v = _rand((2, Hkv * G, Lq, 8), 83), _rand((2, Hkv, Lk, 8), 84), _rand((2, Hkv, Lk, 8), 85)
+    ia = torch.arange(Lq)[:, None] + (Lk - Lq)
+    j = torch.arange(Lk)[None, :]
+    vis = (j <= ia) & (j > ia - W)
+    mask = torch.zeros(Lq, Lk, dtype=torch.float64).masked_fill(~vis, float("-inf"))
+    qt, kt, vt = (torch.from_numpy(x) for x in (q, k, v))
+    kt, vt = kt.repeat_interleave(G, dim=1), vt.repeat_interleave(G, dim=1)
+    ref = F.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask, scale=0.3).numpy()
+    rows_seen = vis.any(dim=1).numpy()
+    o = oracle.attention(q, k, v, scale=0.3, causal=True, window=W)
+    np.testing.assert_allclose(o[:, :, rows_seen], ref[:, :, rows_seen], atol=1e-12)
+    assert np.all(o[:, :, ~rows_seen] == 0)
+
+
+def test_window_needs_the_causal_mask():
+    q = _rand((1, 1, 3, 2), 86)
+    with pytest.raises(ValueError):
+        oracle.attention(q, q, q, scale=1.0, window=2)
