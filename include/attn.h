@@ -70,7 +70,8 @@ typedef enum {
   ATTN_ERR_UNSUPPORTED = -3, /* head dim not 64 or 128, unknown dtype, or (attn_fwd_mod)
                                 softcap or window without the causal mask, or softcap
                                 together with ALiBi */
-  ATTN_ERR_WORKSPACE = -4,   /* decode workspace smaller than attn_decode_workspace_bytes() */
+  ATTN_ERR_WORKSPACE = -4,   /* decode workspace smaller than attn_decode_workspace_bytes(), or
+                                (attn_decode_noalloc) larger than ATTN_DECODE_NOALLOC_BYTES */
   ATTN_ERR_HIP = -5          /* a HIP launch failed; see attn_last_hip_error() */
 } attn_status;
 
@@ -180,6 +181,31 @@ int attn_decode_mod(const void* Q, const void* K, const void* V, void* O,
                     float scale, const float* alibi_slopes, float softcap, int num_splits,
                     void* workspace, size_t workspace_bytes,
                     attn_dtype dtype, hipStream_t stream);
+
+/* Bytes of the static workspace that attn_decode_noalloc uses. */
+#define ATTN_DECODE_NOALLOC_BYTES ((size_t)16 << 20)
+
+/*
+ * attn_decode_mod for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * kernels and results, with the workspace taken from a static device array of
+ * ATTN_DECODE_NOALLOC_BYTES that the library holds on each GPU it runs on
+ * until the process ends.  The caller passes inputs and outputs only.  It
+ * calls no hipMalloc, hipFree or allocating routine; the first call on a
+ * device looks the array's address up (hipGetSymbolAddress) and keeps it.
+ *   Limit: attn_decode_workspace_bytes(B, Hq, D, resolved num_splits) must
+ *   not exceed ATTN_DECODE_NOALLOC_BYTES (ATTN_ERR_WORKSPACE otherwise).
+ *   Every call on a GPU shares that GPU's array, which keeps the last call's
+ *   partials: calls that overlap on one GPU (other streams, other threads)
+ *   race and must be serialised by the caller.  Every partial is written
+ *   before it is read, so nothing has to start at zero.
+ * Errors: as attn_decode_mod (no workspace arguments), ATTN_ERR_WORKSPACE for
+ * the size limit, ATTN_ERR_HIP if the address lookup or a launch fails.
+ */
+int attn_decode_noalloc(const void* Q, const void* K, const void* V, void* O,
+                        int B, int Hq, int Hkv, int Lk, int D,
+                        float scale, const float* alibi_slopes, float softcap, int num_splits,
+                        attn_dtype dtype, hipStream_t stream);
 
 /*
  * The kernels that attn_fwd_mod (attn_fwd: softcap = 0, window = 0) launches

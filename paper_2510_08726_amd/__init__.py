@@ -16,7 +16,7 @@ import torch
 
 __all__ = [
     "attn_fwd", "attn_fwd_mod", "attn_decode", "attn_decode_mod", "attn_decode_workspace_bytes",
-    "attn_decode_num_splits", "attn_fwd_kernels", "attn_decode_kernels",
+    "attn_decode_num_splits", "attn_decode_noalloc", "attn_fwd_kernels", "attn_decode_kernels",
     "attn_status_string", "attn_last_hip_error", "library_path", "load_library", "AttnError",
     "ATTN_OK", "ATTN_ERR_NULL", "ATTN_ERR_SHAPE", "ATTN_ERR_UNSUPPORTED", "ATTN_ERR_WORKSPACE",
     "ATTN_ERR_HIP",
@@ -73,6 +73,8 @@ def load_library():
     lib.attn_decode_workspace_bytes.restype = cs
     lib.attn_decode_num_splits.argtypes = [ci, ci, ci, ci, ci]
     lib.attn_decode_num_splits.restype = ci
+    lib.attn_decode_noalloc.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp, cf, ci, ci, vp]
+    lib.attn_decode_noalloc.restype = ci
     lib.attn_fwd_kernels.argtypes = [ci, ci, ci, ci, cf, ci, ctypes.c_char_p, cs]
     lib.attn_fwd_kernels.restype = ci
     lib.attn_decode_kernels.argtypes = [ci, ci, ci, ci, ci, cf, ctypes.c_char_p, cs]
@@ -237,6 +239,30 @@ def attn_decode_mod(q, k, v, o=None, *, scale=None, alibi_slopes=None, softcap=N
                                           _ptr(alibi_slopes), float(softcap or 0.0), int(num_splits),
                                           _ptr(workspace), workspace.numel() * workspace.element_size(),
                                           _DTYPE_CODE[q.dtype], _stream(stream)))
+    return o
+
+
+ATTN_DECODE_NOALLOC_BYTES = 16 << 20
+
+
+def attn_decode_noalloc(q, k, v, o=None, *, scale=None, alibi_slopes=None, softcap=None, num_splits=0,
+                        stream=None):
+    """attn_decode_mod with the workspace in the library's static device array
+    (no allocation inside the library; ``o`` is allocated here if not given).
+    Calls that overlap on one GPU race on that array."""
+    _check_tensors(q, k, v, alibi_slopes)
+    B, Hq, Lq, D = q.shape
+    _require(Lq == 1, "decode takes one query token (q.shape[2] == 1)")
+    Hkv, Lk = k.shape[1], k.shape[2]
+    _require(k.shape[0] == B and k.shape[3] == D, "k/v batch and head dim must match q")
+    if o is None:
+        o = torch.empty_like(q)
+    _require(o.shape == q.shape and o.dtype == q.dtype and o.is_contiguous() and o.is_cuda,
+             "o must be a contiguous GPU tensor shaped like q")
+    sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    _check(load_library().attn_decode_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, Lk, D, sc,
+                                              _ptr(alibi_slopes), float(softcap or 0.0), int(num_splits),
+                                              _DTYPE_CODE[q.dtype], _stream(stream)))
     return o
 
 

@@ -77,7 +77,7 @@ const char* attn_status_string(int status) {
     case ATTN_ERR_NULL: return "ATTN_ERR_NULL: a required pointer is NULL";
     case ATTN_ERR_SHAPE: return "ATTN_ERR_SHAPE: invalid sizes (need B,Hq,Hkv,Lq,Lk >= 1, Hq % Hkv == 0, num_splits >= 0, window >= 0, finite scale, finite softcap >= 0)";
     case ATTN_ERR_UNSUPPORTED: return "ATTN_ERR_UNSUPPORTED: head dim must be 64 or 128 and dtype ATTN_F16 or ATTN_BF16; softcap and window need the causal mask, softcap excludes ALiBi";
-    case ATTN_ERR_WORKSPACE: return "ATTN_ERR_WORKSPACE: decode workspace too small";
+    case ATTN_ERR_WORKSPACE: return "ATTN_ERR_WORKSPACE: decode workspace too small (attn_decode_noalloc: the split count needs more than its 16 MiB static workspace)";
     case ATTN_ERR_HIP: return "ATTN_ERR_HIP: a HIP launch failed (see attn_last_hip_error)";
     default: return "unknown attn_status";
   }
@@ -160,23 +160,30 @@ size_t attn_decode_workspace_bytes(int B, int Hq, int D, int num_splits) {
   return (bytes + 255) & ~(size_t)255;
 }
 
-int attn_decode_mod(const void* Q, const void* K, const void* V, void* O,
-                int B, int Hq, int Hkv, int Lk, int D,
-                float scale, const float* alibi_slopes, float softcap, int num_splits,
-                void* workspace, size_t workspace_bytes,
-                attn_dtype dtype, hipStream_t stream) {
-  if (!Q || !K || !V || !O || !workspace) return ATTN_ERR_NULL;
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the decode entry points (everything but the workspace);
+// on success *S is the resolved chunk count.
+int decode_check(const void* Q, const void* K, const void* V, void* O, int B, int Hq, int Hkv, int Lk, int D,
+                 float scale, float softcap, int num_splits, attn_dtype dtype, int* S) {
+  if (!Q || !K || !V || !O) return ATTN_ERR_NULL;
   if (!shape_ok(B, Hq, Hkv, 1, Lk) || num_splits < 0 || !std::isfinite(scale)) return ATTN_ERR_SHAPE;
   if (!std::isfinite(softcap) || softcap < 0.f) return ATTN_ERR_SHAPE;
   if (!dims_supported(D, dtype)) return ATTN_ERR_UNSUPPORTED;
   if (!sizes_fit(B, Hq, Hkv, 1, Lk, D)) return ATTN_ERR_SHAPE;
-  const int S = num_splits ? num_splits : attn_decode_num_splits(B, Hq, Hkv, Lk, D);
+  *S = num_splits ? num_splits : attn_decode_num_splits(B, Hq, Hkv, Lk, D);
   const int group = Hq / Hkv;
-  const int64_t nblocks = (int64_t)S * (group / decode_heads_per_block(group)) * Hkv * B;
+  const int64_t nblocks = (int64_t)*S * (group / decode_heads_per_block(group)) * Hkv * B;
   if (nblocks > kMaxGrid || (int64_t)B * Hq > kMaxGrid) return ATTN_ERR_SHAPE;
-  const size_t need = attn_decode_workspace_bytes(B, Hq, D, S);
-  if (workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 15)) return ATTN_ERR_WORKSPACE;
+  return ATTN_OK;
+}
 
+// Launch the split and combine kernels with a checked workspace.
+int decode_launch(const void* Q, const void* K, const void* V, void* O, int B, int Hq, int Hkv, int Lk, int D,
+                  float scale, const float* alibi_slopes, float softcap, int S, void* workspace, attn_dtype dtype,
+                  hipStream_t stream) {
   attn::DecodeParams p{};
   p.q = Q; p.k = K; p.v = V; p.o = O;
   p.slopes = alibi_slopes;
@@ -185,7 +192,7 @@ int attn_decode_mod(const void* Q, const void* K, const void* V, void* O,
   p.ws_m = p.ws_o + n * D;
   p.ws_l = p.ws_m + n;
   p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Lk = Lk; p.D = D;
-  p.group = group;
+  p.group = Hq / Hkv;
   p.splits = S;
   p.chunk = (Lk + S - 1) / S;
   p.bf16 = dtype == ATTN_BF16;
@@ -194,6 +201,38 @@ int attn_decode_mod(const void* Q, const void* K, const void* V, void* O,
   p.cap_cl = softcap > 0.f ? softcap * kLog2e : 0.f;
   hipError_t e = attn::launch_decode(p, stream);
   return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int attn_decode_mod(const void* Q, const void* K, const void* V, void* O,
+                    int B, int Hq, int Hkv, int Lk, int D,
+                    float scale, const float* alibi_slopes, float softcap, int num_splits,
+                    void* workspace, size_t workspace_bytes,
+                    attn_dtype dtype, hipStream_t stream) {
+  int S = 0;
+  const int rc = decode_check(Q, K, V, O, B, Hq, Hkv, Lk, D, scale, softcap, num_splits, dtype, &S);
+  if (rc != ATTN_OK) return rc;
+  if (!workspace) return ATTN_ERR_NULL;
+  const size_t need = attn_decode_workspace_bytes(B, Hq, D, S);
+  if (workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 15)) return ATTN_ERR_WORKSPACE;
+  return decode_launch(Q, K, V, O, B, Hq, Hkv, Lk, D, scale, alibi_slopes, softcap, S, workspace, dtype, stream);
+}
+
+int attn_decode_noalloc(const void* Q, const void* K, const void* V, void* O,
+                        int B, int Hq, int Hkv, int Lk, int D,
+                        float scale, const float* alibi_slopes, float softcap, int num_splits,
+                        attn_dtype dtype, hipStream_t stream) {
+  int S = 0;
+  const int rc = decode_check(Q, K, V, O, B, Hq, Hkv, Lk, D, scale, softcap, num_splits, dtype, &S);
+  if (rc != ATTN_OK) return rc;
+  if (attn_decode_workspace_bytes(B, Hq, D, S) > attn::kDecodeScratchBytes) return ATTN_ERR_WORKSPACE;
+  void* ws = nullptr;
+  const hipError_t e = attn::decode_scratch(&ws);
+  if (e != hipSuccess) return hip_fail(e);
+  return decode_launch(Q, K, V, O, B, Hq, Hkv, Lk, D, scale, alibi_slopes, softcap, S, ws, dtype, stream);
 }
 
 int attn_decode(const void* Q, const void* K, const void* V, void* O,

@@ -19,12 +19,22 @@
 // keeps its own online-softmax state over its keys; the groups are merged
 // once at the end.
 
+#include <mutex>
+
 #include "kernel_common.h"
 #include "launch.h"
 
 namespace attn {
 
 namespace {
+
+// Decode workspace of attn_decode_noalloc, for callers that cannot allocate:
+// one array per device, loaded with this code object and held until the
+// process ends.  Host code never passes the array's name to a kernel (on the
+// host it is only a stand-in); it uses the device address that
+// hipGetSymbolAddress returns for the current device, kept per device.
+static __device__ __align__(256) char scratch[kDecodeScratchBytes];
+constexpr int kMaxDevices = 64;
 
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;  // keys per lane group per step (loads in flight)
@@ -553,6 +563,20 @@ hipError_t launch_g(const DecodeParams& p, hipStream_t stream) {
 }
 
 }  // namespace
+
+hipError_t decode_scratch(void** ptr) {
+  static std::once_flag once[kMaxDevices];
+  static void* addr[kMaxDevices];
+  static hipError_t err[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::call_once(once[dev], [dev] { err[dev] = hipGetSymbolAddress(&addr[dev], HIP_SYMBOL(scratch)); });
+  if (err[dev] != hipSuccess) return err[dev];
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
   if (p.D == 64) return p.bf16 ? launch_g<64, __bf16>(p, stream) : launch_g<64, _Float16>(p, stream);

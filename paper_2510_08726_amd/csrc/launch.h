@@ -77,4 +77,10 @@ hipError_t launch_prefill_d64_f16(const PrefillParams& p, hipStream_t stream);
 hipError_t launch_prefill_d64_bf16(const PrefillParams& p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
 
+// Bytes of the static decode workspace of attn_decode_noalloc.
+constexpr size_t kDecodeScratchBytes = size_t(16) << 20;
+// Device address of that workspace on the current device (resolved once per
+// device, then cached).
+hipError_t decode_scratch(void** ptr);
+
 }  // namespace attn
