@@ -1,29 +1,33 @@
-"""Benchmark of the fused attention hot path on one MI355X.
+"""Benchmark of the fused attention hot path (and the paper's row reductions) on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--only NAME] [--no-cpu-baseline]
+                    [--no-errors] [--no-peaks]
 
-A step is one call of the library on one batch of the workload: attn_fwd for a
-prefill workload (one kernel), attn_decode for a decode workload (split kernel
-+ combine kernel).  W untimed steps, then K steps timed with HIP events on the
-stream the kernels are launched on, bracketed by device synchronisation.  All
-inputs are resident in HBM before the timed region.
+A step is one call of the library on one batch of a workload: attn_fwd(_mod)
+for a prefill workload (one kernel), attn_decode(_mod) for a decode workload
+(split kernel + combine kernel), norm_l2 / rmsnorm_rowmax for a row reduction
+(split kernel + combine kernel).  W untimed steps, then K steps timed with HIP
+events recorded on the stream the kernels are launched on (the current torch
+stream, which the binding passes to the library), bracketed by device
+synchronisation.  All inputs are resident in HBM before the timed region.
 
 The headline line is the causal MHA prefill workload (B=4, H=32, L=2048,
 D=128, fp16): `value` is its algorithmic TFLOP/s (4*D per visible query/key
-pair).  The decode workloads (B=8, H=32, Lk=8192, D=128; and B=16, Hq=32,
-Hkv=8, Lk=32768, D=128) are reported beside it in `decode` and `decode_gqa` as
-algorithmic GB/s (|Q|+|K|+|V|+|O|), the ALiBi decode workload (the MHA decode
-shape with the ALiBi bias) in `decode_alibi`, the SoftCap decode workload (B=16,
-Hq=32, Hkv=16, Lk=8192, D=128, cap 50) in `decode_softcap`, the SoftCap causal
-prefill (B=2, Hq=32, Hkv=16, L=4096, D=128, cap 50) in `prefill_softcap`, and
-every workload is listed under `workloads`.  `cpu_baseline` is the fp64 oracle timed on this host on a
-bounded sample of the headline workload.
+pair) and `roofline` its MFMA roofline, against the published dense fp16 peak
+and against the peak that an MFMA loop on random operands reaches on the same
+GPU in the same run (`achievable`, with the shader clock it held).  Beside it:
+the decode workloads as algorithmic GB/s (|Q|+|K|+|V|+|O|) against the HBM
+peak and the measured streaming-read rate, the other prefill workloads, a
+decode split-count sweep, the row reductions, error metrics of every workload
+against the fp64 oracle (max, mean, RMS, p90, p99 of |GPU - oracle| on a
+stated sample), and `cpu_baseline`: the oracle timed on this host.
 """
 
 import argparse
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -33,17 +37,22 @@ sys.path.insert(0, ROOT)
 MFMA_PEAK_TFLOPS = 2500.0    # MI355X dense fp16/bf16 MFMA, published
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 HEADLINE = "causal_mha_prefill"
-DECODE_HEADLINE = "mha_decode"
-DECODE_GQA = "gqa_long_decode"
-DECODE_ALIBI = "alibi_decode"
-DECODE_SOFTCAP = "softcap_decode"
-PREFILL_SOFTCAP = "softcap_causal_prefill"
 METRIC = "prefill attn TFLOP/s (% MFMA peak); decode KV-read GB/s (% HBM peak)"
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
     "prefill": ["prefill.hip", "kernel_common.h", "launch.h"],
     "decode": ["decode.hip", "kernel_common.h", "launch.h"],
+    "norms": ["norms.hip", "kernel_common.h", "launch.h"],
 }
+# bench-line keys of the workloads reported beside the headline
+SIDE = {
+    "decode": "mha_decode", "decode_gqa": "gqa_long_decode", "decode_alibi": "alibi_decode",
+    "decode_softcap": "softcap_decode", "prefill_gqa": "gqa_causal_prefill",
+    "prefill_alibi": "alibi_causal_prefill", "prefill_softcap": "softcap_causal_prefill",
+    "prefill_window": "window_causal_prefill",
+}
+SWEEP_WORKLOAD = "mha_decode"
+SWEEP_SPLITS = (16, 32, 64)
 
 
 def kernel_source_hash(kind):
@@ -54,9 +63,9 @@ def kernel_source_hash(kind):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kind, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
-    when it is missing or was taken on a different version of the kernel."""
+def _profile_entry(kind, workload):
+    """The committed rocprofv3 counter summary of a workload, or None when it
+    is missing or was taken on a different version of the kernels."""
     path = os.path.join(PROFILES, "traffic.json")
     if not os.path.exists(path):
         return None
@@ -65,20 +74,19 @@ def measured_traffic(kind, workload):
     ent = data.get(f"{kind}:{workload}")
     if not ent or ent.get("source_hash") != kernel_source_hash(kind):
         return None
-    return ent.get("traffic_bytes_per_step")
+    return ent
 
 
-def decode_entry(name, dec):
-    """The decode workload's throughput and its HBM roofline (split + combine kernels)."""
-    return {
-        "workload": name, "value": dec["GB/s"], "unit": "GB/s",
-        "ms_per_step": dec["ms_per_step"], "num_splits": dec["num_splits"],
-        "roofline": {"bound": "hbm", "achieved": dec["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dec["GB/s"] / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("decode", name),
-                     "per_launch": f"{dec['bytes_per_step']} algorithmic bytes (|Q|+|K|+|V|+|O|), "
-                                   "split + combine kernels"},
-    }
+def measured_traffic(kind, workload):
+    ent = _profile_entry(kind, workload)
+    return None if ent is None else ent.get("traffic_bytes_per_step")
+
+
+def measured_mfma_busy(workload):
+    """MFMA-busy fraction of SIMD cycles (SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE x SIMDs) from the committed counter profile, or None."""
+    ent = _profile_entry("prefill", workload)
+    return None if ent is None else ent.get("mfma_busy")
 
 
 def parse():
@@ -87,11 +95,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--only", default=None, help="run only this workload (for profiler passes)")
+    ap.add_argument("--splits", type=int, default=0, help="decode split count with --only (0: library)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-errors", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="budget of the oracle timing sample")
+                    help="budget of the headline oracle timing sample")
     return ap.parse_args()
 
 
@@ -112,7 +123,40 @@ def time_steps(fn, steps, warmup):
     return start.elapsed_time(end) / steps, wall
 
 
-def run_workload(name, steps, warmup):
+def _error_stats(got, ref):
+    import numpy as np
+    d = np.abs(np.asarray(got, dtype=np.float64) - ref).ravel()
+    return {"max_abs": float(d.max()), "mean_abs": float(d.mean()), "rms": float(np.sqrt(np.mean(d * d))),
+            "p90": float(np.percentile(d, 90)), "p99": float(np.percentile(d, 99))}
+
+
+def attention_errors(w, q, k, v, sl, o):
+    """|GPU - oracle| on a sample: prefill, two (batch, head) slices (the first
+    and the last) on every row for L <= 4096, else on the first and last row of
+    every 32-row block; decode, every row."""
+    import numpy as np
+    import oracle
+    qn, kn, vn = (t.cpu().float().numpy() for t in (q, k, v))
+    sln = None if sl is None else sl.cpu().double().numpy()
+    og = o.cpu().float().numpy()
+    if w.decode:
+        ref = oracle.attention(qn, kn, vn, scale=w.sm_scale, causal=True, alibi_slopes=sln,
+                               softcap=w.softcap or None)
+        return {**_error_stats(og, ref), "sample": "every output row"}
+    heads = sorted({(0, 0), (w.B - 1, w.Hq - 1)})
+    rows = None
+    if w.Lq > 4096:
+        rows = sorted({r for r0 in range(0, w.Lq, 32) for r in (r0, min(r0 + 31, w.Lq - 1))})
+    ref = oracle.attention(qn, kn, vn, scale=w.sm_scale, causal=w.causal, alibi_slopes=sln,
+                           softcap=w.softcap or None, window=w.window or None, rows=rows, heads=heads)
+    got = og if rows is None else og[:, :, rows]
+    b = [h[0] for h in heads]
+    hq = [h[1] for h in heads]
+    sample = f"(batch, head) {heads}, " + ("every row" if rows is None else "first/last row of every 32-row block")
+    return {**_error_stats(got[b, hq], ref[b, hq]), "sample": sample}
+
+
+def run_workload(name, steps, warmup, *, splits=0, errors=False):
     import torch
     import paper_2510_08726_amd as pa
     from paper_2510_08726_amd.workloads import WORKLOADS, make_inputs, prefill_flops, decode_bytes
@@ -121,7 +165,7 @@ def run_workload(name, steps, warmup):
     q, k, v, sl = make_inputs(w, device="cuda")
     o = torch.empty_like(q)
     if w.decode:
-        S = w.num_splits or pa.attn_decode_num_splits(w.B, w.Hq, w.Hkv, w.Lk, w.D)
+        S = splits or w.num_splits or pa.attn_decode_num_splits(w.B, w.Hq, w.Hkv, w.Lk, w.D)
         ws = torch.empty(pa.attn_decode_workspace_bytes(w.B, w.Hq, w.D, S), dtype=torch.uint8,
                          device="cuda")
 
@@ -129,6 +173,7 @@ def run_workload(name, steps, warmup):
             pa.attn_decode(q, k, v, o, scale=w.sm_scale, alibi_slopes=sl, softcap=w.softcap or None,
                            num_splits=S, workspace=ws)
         work = decode_bytes(w.B, w.Hq, w.Hkv, w.Lk, w.D)
+        kernels = pa.attn_decode_kernels(w.Hq, w.Hkv, w.D, q.dtype, sl is not None, w.softcap)
     else:
         S = None
 
@@ -136,12 +181,12 @@ def run_workload(name, steps, warmup):
             pa.attn_fwd(q, k, v, o, causal=w.causal, scale=w.sm_scale, alibi_slopes=sl,
                         softcap=w.softcap or None, window=w.window or None)
         work = prefill_flops(w.B, w.Hq, w.Lq, w.Lk, w.D, w.causal, w.window)
+        kernels = pa.attn_fwd_kernels(w.D, q.dtype, w.causal, sl is not None, w.softcap, w.window)
     ms, wall_ms = time_steps(fn, steps, warmup)
     res = {
         "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk, "D": w.D, "dtype": w.dtype,
         "causal": w.causal, "alibi": w.alibi, "softcap": w.softcap, "window": w.window,
-        "ms_per_step": round(ms, 5),
-        "host_wall_ms_per_step": round(wall_ms, 5),
+        "kernels": kernels, "ms_per_step": round(ms, 5), "host_wall_ms_per_step": round(wall_ms, 5),
     }
     if w.decode:
         gbs = work / (ms * 1e-3) / 1e9
@@ -151,9 +196,113 @@ def run_workload(name, steps, warmup):
         tf = work / (ms * 1e-3) / 1e12
         res.update({"flops_per_step": work, "TFLOP/s": round(tf, 2),
                     "pct_mfma_peak": round(100 * tf / MFMA_PEAK_TFLOPS, 2)})
+    err = attention_errors(w, q, k, v, sl, o) if errors else None
     del q, k, v, o
     torch.cuda.empty_cache()
-    return res
+    return res, err
+
+
+def run_norm(name, steps, warmup, *, errors=False):
+    import numpy as np
+    import torch
+    import paper_2510_08726_amd as pa
+    from paper_2510_08726_amd.workloads import NORM_WORKLOADS, make_norm_input, norm_bytes
+
+    w = NORM_WORKLOADS[name]
+    x = make_norm_input(w, device="cuda")
+    C = pa.norm_chunks(w.N, w.M, x.dtype)
+    ws = torch.empty(pa.norm_workspace_bytes(w.N, C), dtype=torch.uint8, device="cuda")
+    out = torch.empty(w.N, dtype=torch.float32, device="cuda")
+    if w.op == "l2":
+        def fn():
+            pa.norm_l2(x, out, chunks=C, workspace=ws)
+    else:
+        y = torch.empty_like(x)
+
+        def fn():
+            pa.rmsnorm_rowmax(x, y, out, eps=w.eps, chunks=C, workspace=ws)
+    ms, wall_ms = time_steps(fn, steps, warmup)
+    work = norm_bytes(w.op, w.N, w.M, x.element_size())
+    gbs = work / (ms * 1e-3) / 1e9
+    res = {"op": w.op, "N": w.N, "M": w.M, "dtype": w.dtype, "chunks": C, "ms_per_step": round(ms, 5),
+           "host_wall_ms_per_step": round(wall_ms, 5), "bytes_per_step": work, "GB/s": round(gbs, 1),
+           "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)}
+    err = None
+    if errors:
+        from oracle import norms
+        x64 = x.cpu().double().numpy()
+        if w.op == "l2":
+            err = {**_error_stats(out.cpu().numpy(), norms.l2_norm(x64)), "sample": "every row norm"}
+        else:
+            yr, mr = norms.rmsnorm_rowmax(x64, w.eps)
+            err = {"y": {**_error_stats(y.cpu().float().numpy(), yr), "sample": "every element of y"},
+                   "rowmax": {**_error_stats(out.cpu().numpy(), mr), "sample": "every row max"}}
+    del x
+    torch.cuda.empty_cache()
+    return res, err
+
+
+def achievable_peaks():
+    """What this GPU reaches in this run: a streaming read of 2 GiB (the
+    decode bound) and the MFMA loop on random fp16 / bf16 operands (the
+    prefill bound), with the shader clock the loop held."""
+    import torch
+    import paper_2510_08726_amd as pa
+    out = {}
+    buf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    buf.view(torch.float32).normal_()
+    sink = pa.peaks_hbm_read(buf)
+    torch.cuda.synchronize()
+    ms, _ = time_steps(lambda: pa.peaks_hbm_read(buf, sink), 10, 2)
+    out["hbm_read_GBs"] = round(buf.numel() / (ms * 1e-3) / 1e9, 1)
+    out["hbm_read_frac_of_spec"] = round(out["hbm_read_GBs"] / HBM_PEAK_GBS, 4)
+    del buf, sink
+    ops = torch.randn(pa.peaks_mfma_operand_bytes() // 2, device="cuda")
+    iters = 20000
+    for dt, key in ((torch.float16, "f16"), (torch.bfloat16, "bf16")):
+        o = ops.to(dt)
+        pa.peaks_mfma(dt, 200, o)
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        _, ck = pa.peaks_mfma(dt, iters, o)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e)
+        flops = pa.peaks_mfma_waves() * iters * 16 * 32768
+        c = ck.cpu().tolist()
+        out[f"mfma_{key}_TFLOPs"] = round(flops / (ms * 1e-3) / 1e12, 1)
+        out[f"mfma_{key}_frac_of_spec"] = round(out[f"mfma_{key}_TFLOPs"] / MFMA_PEAK_TFLOPS, 4)
+        out[f"mfma_{key}_clock_GHz"] = round(c[0] / c[1] * 0.1, 3) if c[1] else None
+    out["method"] = ("peaks_hbm_read over 2 GiB (10 launches); peaks_mfma: 32x32x16 MFMAs on operands "
+                     "that change every instruction, 2 waves per SIMD, 20000 x 16 per wave; clock from "
+                     "s_memtime / s_memrealtime")
+    return out
+
+
+def prefill_roofline(res, name, peaks, kernel):
+    tf = res["TFLOP/s"]
+    r = {"bound": "mfma", "achieved": tf, "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+         "frac": round(tf / MFMA_PEAK_TFLOPS, 4), "traffic": measured_traffic("prefill", name),
+         "kernel": kernel,
+         "per_launch": f"{res['flops_per_step']} algorithmic flops (4*D per visible query/key pair), one launch",
+         "mfma_busy_counter": measured_mfma_busy(name)}
+    key = "mfma_bf16_TFLOPs" if res["dtype"] == "bf16" else "mfma_f16_TFLOPs"
+    if peaks and peaks.get(key):
+        r["achievable_peak"] = peaks[key]
+        r["frac_achievable"] = round(tf / peaks[key], 4)
+    return r
+
+
+def hbm_roofline(res, kind, name, peaks, what):
+    gbs = res["GB/s"]
+    r = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+         "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(kind, name),
+         "per_launch": f"{res['bytes_per_step']} algorithmic bytes ({what})"}
+    if peaks and peaks.get("hbm_read_GBs"):
+        r["achievable_peak"] = peaks["hbm_read_GBs"]
+        r["frac_achievable"] = round(gbs / peaks["hbm_read_GBs"], 4)
+    return r
 
 
 def copy_calibration(mib, steps):
@@ -167,37 +316,86 @@ def copy_calibration(mib, steps):
     torch.cuda.synchronize()
 
 
-def cpu_baseline(budget_s):
-    """The fp64 oracle on whole (batch, head) slices of the headline workload."""
-    import numpy as np
-    import oracle
-    from paper_2510_08726_amd.workloads import WORKLOADS, make_inputs, prefill_flops
+def _host():
+    model = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     try:
         import threadpoolctl
         info = threadpoolctl.threadpool_info()
-        cores = max([d.get("num_threads", 1) for d in info if d.get("user_api") == "blas"] or [1])
+        blas = max([d.get("num_threads", 1) for d in info if d.get("user_api") == "blas"] or [1])
     except Exception:
-        cores = 1
-    w = WORKLOADS[HEADLINE]
-    q, k, v, _ = make_inputs(w)
-    qn, kn, vn = (t.float().numpy() for t in (q, k, v))
-    heads = [(b, h) for b in range(w.B) for h in range(w.Hq)]
-    done = 0
-    t0 = time.perf_counter()
-    for bh in heads:
-        oracle.attention(qn, kn, vn, scale=w.sm_scale, causal=w.causal, heads=[bh])
-        done += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    el = time.perf_counter() - t0
-    flops = prefill_flops(1, done, w.Lq, w.Lk, w.D, w.causal)
+        blas = 1
+    return model, os.cpu_count(), int(blas)
+
+
+def cpu_baseline(budget_s):
+    """The fp64 oracle timed on this host: whole (batch, head) slices of the
+    headline workload for about `budget_s`, and a bounded sample of every
+    other workload, each in its metric's unit."""
+    import numpy as np
+    import oracle
+    from oracle import norms
+    from paper_2510_08726_amd.workloads import (WORKLOADS, NORM_WORKLOADS, make_inputs, make_norm_input,
+                                                prefill_flops, decode_bytes, norm_bytes)
+    model, ncpu, cores = _host()
+
+    def prefill_sample(w, budget, max_slices):
+        q, k, v, sl = make_inputs(w)
+        qn, kn, vn = (t.float().numpy() for t in (q, k, v))
+        sln = None if sl is None else sl.double().numpy()
+        heads = [(b, h) for b in range(w.B) for h in range(w.Hq)]
+        done, t0 = 0, time.perf_counter()
+        for bh in heads[:max_slices]:
+            oracle.attention(qn, kn, vn, scale=w.sm_scale, causal=w.causal, alibi_slopes=sln,
+                             softcap=w.softcap or None, window=w.window or None, heads=[bh])
+            done += 1
+            if time.perf_counter() - t0 >= budget:
+                break
+        el = time.perf_counter() - t0
+        flops = prefill_flops(1, done, w.Lq, w.Lk, w.D, w.causal, w.window)
+        return flops / el / 1e12, el, f"{done} of {len(heads)} (batch, head) slices, every query row"
+
+    head_tf, head_el, head_sample = prefill_sample(WORKLOADS[HEADLINE], budget_s, 1 << 30)
+    per = {}
+    for name, w in WORKLOADS.items():
+        if name == HEADLINE:
+            continue
+        if w.decode:
+            q, k, v, sl = make_inputs(w)
+            b = 1
+            qn, kn, vn = (t[:b].float().numpy() for t in (q, k, v))
+            t0 = time.perf_counter()
+            oracle.attention(qn, kn, vn, scale=w.sm_scale, causal=True,
+                             alibi_slopes=None if sl is None else sl.double().numpy(), softcap=w.softcap or None)
+            el = time.perf_counter() - t0
+            per[name] = {"value": round(decode_bytes(b, w.Hq, w.Hkv, w.Lk, w.D) / el / 1e9, 4), "unit": "GB/s",
+                         "sample": f"batch 0 of {w.B}, every head", "seconds": round(el, 2)}
+        else:
+            tf, el, sample = prefill_sample(w, 2.0, 2)
+            per[name] = {"value": round(tf, 6), "unit": "TFLOP/s", "sample": sample, "seconds": round(el, 2)}
+    for name, w in NORM_WORKLOADS.items():
+        x = make_norm_input(w)[:32].double().numpy()
+        t0 = time.perf_counter()
+        if w.op == "l2":
+            norms.l2_norm(x)
+        else:
+            norms.rmsnorm_rowmax(x, w.eps)
+        el = time.perf_counter() - t0
+        per[name] = {"value": round(norm_bytes(w.op, 32, w.M, 2 if w.dtype != "f32" else 4) / el / 1e9, 4),
+                     "unit": "GB/s", "sample": f"32 of {w.N} rows", "seconds": round(el, 4)}
     return {
-        "value": round(flops / el / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores),
-        "kind": "oracle",
-        "sample": f"{done} of {len(heads)} (batch, head) slices of {HEADLINE}, all {w.Lq} query rows "
-                  f"each, float64 numpy (BLAS matmul on {cores} threads, exp single-threaded); "
-                  f"{el:.1f} s",
-        "seconds": round(el, 2),
+        "value": round(head_tf, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+        "sample": f"{head_sample} of {HEADLINE}; float64 numpy, BLAS matmul on {cores} threads, exp "
+                  f"single-threaded; {head_el:.1f} s",
+        "seconds": round(head_el, 2), "cpu_model": model, "nproc": ncpu,
+        "per_config": per,
     }
 
 
@@ -209,45 +407,41 @@ def main():
         sys.exit(2)
     import torch
     import paper_2510_08726_amd as pa
-    from paper_2510_08726_amd.workloads import WORKLOADS
+    from paper_2510_08726_amd.workloads import WORKLOADS, NORM_WORKLOADS
     pa.load_library()
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
 
     if args.only:
-        res = run_workload(args.only, args.steps, args.warmup)
+        if args.only in NORM_WORKLOADS:
+            res, _ = run_norm(args.only, args.steps, args.warmup)
+        else:
+            res, _ = run_workload(args.only, args.steps, args.warmup, splits=args.splits)
         if args.copy_mib:
             copy_calibration(args.copy_mib, args.steps)
         print(json.dumps({"workload": args.only, **res}), flush=True)
         return
 
-    results = {}
+    peaks = None if args.no_peaks else achievable_peaks()
+    print(f"# achievable: {json.dumps(peaks)}", file=sys.stderr, flush=True)
+    results, errors = {}, {}
     for name in WORKLOADS:
-        results[name] = run_workload(name, args.steps, args.warmup)
+        results[name], errors[name] = run_workload(name, args.steps, args.warmup, errors=not args.no_errors)
         print(f"# {name}: {json.dumps(results[name])}", file=sys.stderr, flush=True)
+    for name in NORM_WORKLOADS:
+        results[name], errors[name] = run_norm(name, args.steps, args.warmup, errors=not args.no_errors)
+        print(f"# {name}: {json.dumps(results[name])}", file=sys.stderr, flush=True)
+    sweep = {}
+    for S in SWEEP_SPLITS:
+        r, _ = run_workload(SWEEP_WORKLOAD, args.steps, args.warmup, splits=S)
+        sweep[str(S)] = {"GB/s": r["GB/s"], "ms_per_step": r["ms_per_step"],
+                         "frac": round(r["GB/s"] / HBM_PEAK_GBS, 4),
+                         "frac_achievable": round(r["GB/s"] / peaks["hbm_read_GBs"], 4) if peaks else None}
+    print(f"# split sweep: {json.dumps(sweep)}", file=sys.stderr, flush=True)
 
     head = results[HEADLINE]
     w = WORKLOADS[HEADLINE]
-    traffic = measured_traffic("prefill", HEADLINE)
-    roofline = {
-        "bound": "mfma", "achieved": head["TFLOP/s"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-        "frac": round(head["TFLOP/s"] / MFMA_PEAK_TFLOPS, 4), "traffic": traffic,
-        "kernel": "prefill_kernel<128, f16, causal>",
-        "per_launch": f"{head['flops_per_step']} algorithmic flops (4*D per visible query/key pair)",
-    }
-    decode = decode_entry(DECODE_HEADLINE, results[DECODE_HEADLINE])
-    decode_gqa = decode_entry(DECODE_GQA, results[DECODE_GQA])
-    decode_alibi = decode_entry(DECODE_ALIBI, results[DECODE_ALIBI])
-    decode_softcap = decode_entry(DECODE_SOFTCAP, results[DECODE_SOFTCAP])
-    ps = results[PREFILL_SOFTCAP]
-    prefill_softcap = {
-        "workload": PREFILL_SOFTCAP, "value": ps["TFLOP/s"], "unit": "TFLOP/s", "ms_per_step": ps["ms_per_step"],
-        "roofline": {"bound": "mfma", "achieved": ps["TFLOP/s"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(ps["TFLOP/s"] / MFMA_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic("prefill", PREFILL_SOFTCAP),
-                     "per_launch": f"{ps['flops_per_step']} algorithmic flops (4*D per visible query/key pair)"},
-    }
     line = {
         "metric": METRIC, "value": head["TFLOP/s"], "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
@@ -255,14 +449,28 @@ def main():
         "data": "synthetic",
         "config": {"workload": HEADLINE, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk,
                    "D": w.D, "causal": w.causal, "input": "iid N(0,1) fp16, seed 2"},
-        "roofline": roofline,
-        "decode": decode,
-        "decode_gqa": decode_gqa,
-        "decode_alibi": decode_alibi,
-        "decode_softcap": decode_softcap,
-        "prefill_softcap": prefill_softcap,
-        "workloads": results,
+        "roofline": prefill_roofline(head, HEADLINE, peaks, head["kernels"][0]),
     }
+    for key, name in SIDE.items():
+        r = results[name]
+        if WORKLOADS[name].decode:
+            entry = {"workload": name, "value": r["GB/s"], "unit": "GB/s", "ms_per_step": r["ms_per_step"],
+                     "num_splits": r["num_splits"],
+                     "roofline": hbm_roofline(r, "decode", name, peaks, "|Q|+|K|+|V|+|O|, split + combine kernels")}
+        else:
+            entry = {"workload": name, "value": r["TFLOP/s"], "unit": "TFLOP/s", "ms_per_step": r["ms_per_step"],
+                     "roofline": prefill_roofline(r, name, peaks, r["kernels"][0])}
+        line[key] = entry
+    line["decode_split_sweep"] = {"workload": SWEEP_WORKLOAD, "splits": sweep}
+    line["norms"] = {name: {"workload": name, "value": results[name]["GB/s"], "unit": "GB/s",
+                            "ms_per_step": results[name]["ms_per_step"],
+                            "roofline": hbm_roofline(results[name], "norms", name, peaks,
+                                                     "X read once + the [N] fp32 outputs (+ Y written, RMSNorm)")}
+                     for name in NORM_WORKLOADS}
+    line["achievable"] = peaks
+    if not args.no_errors:
+        line["errors"] = errors
+    line["workloads"] = results
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -26,6 +26,12 @@ Contents
                    have the same meaning as the decode kernel's partials, so the
                    GPU workspace can be compared with them element by element.
 
+``norms``          the row reductions of the paper's second workload (stable
+                   L2 norm; RMSNorm and the row max of its output, Section
+                   "Example Operators Amenable to Neptune Transformations"):
+                   plain definitions, plus their single-pass (rolling) and
+                   split-k forms.
+
 Parity status: every function here is pinned by ``tests/test_oracle_pins.py``
 and ``tests/test_algorithms.py`` (invariants, closed forms, brute force and
 the CPU float64 ``scaled_dot_product_attention`` of PyTorch as a library
@@ -33,4 +39,4 @@ special case).  No function is "parity unpinned".
 """
 
 from .attention import attention, scores, softmax_probs  # noqa: F401
-from . import rolling, splitk  # noqa: F401
+from . import norms, rolling, splitk  # noqa: F401

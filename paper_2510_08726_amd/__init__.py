@@ -16,7 +16,8 @@ import torch
 
 __all__ = [
     "attn_fwd", "attn_fwd_mod", "attn_decode", "attn_decode_mod", "attn_decode_workspace_bytes",
-    "attn_decode_num_splits", "attn_decode_noalloc", "attn_fwd_kernels", "attn_decode_kernels",
+    "attn_decode_num_splits", "attn_decode_noalloc", "peaks_hbm_read", "peaks_mfma", "peaks_mfma_waves",
+    "peaks_mfma_operand_bytes", "norm_chunks", "norm_workspace_bytes", "norm_l2", "rmsnorm_rowmax", "attn_fwd_kernels", "attn_decode_kernels",
     "attn_status_string", "attn_last_hip_error", "library_path", "load_library", "AttnError",
     "ATTN_OK", "ATTN_ERR_NULL", "ATTN_ERR_SHAPE", "ATTN_ERR_UNSUPPORTED", "ATTN_ERR_WORKSPACE",
     "ATTN_ERR_HIP",
@@ -79,6 +80,24 @@ def load_library():
     lib.attn_fwd_kernels.restype = ci
     lib.attn_decode_kernels.argtypes = [ci, ci, ci, ci, ci, cf, ctypes.c_char_p, cs]
     lib.attn_decode_kernels.restype = ci
+    lib.peaks_hbm_read.argtypes = [vp, cs, vp, vp]
+    lib.peaks_hbm_read.restype = ci
+    lib.peaks_hbm_read_sink_floats.argtypes = []
+    lib.peaks_hbm_read_sink_floats.restype = ci
+    lib.peaks_mfma.argtypes = [ci, ci, vp, vp, vp, vp]
+    lib.peaks_mfma.restype = ci
+    lib.peaks_mfma_waves.argtypes = []
+    lib.peaks_mfma_waves.restype = ci
+    lib.peaks_mfma_operand_bytes.argtypes = []
+    lib.peaks_mfma_operand_bytes.restype = cs
+    lib.norm_chunks.argtypes = [ci, ci, ci]
+    lib.norm_chunks.restype = ci
+    lib.norm_workspace_bytes.argtypes = [ci, ci]
+    lib.norm_workspace_bytes.restype = cs
+    lib.norm_l2.argtypes = [vp, vp, ci, ci, ci, ci, vp, cs, vp]
+    lib.norm_l2.restype = ci
+    lib.rmsnorm_rowmax.argtypes = [vp, vp, vp, ci, ci, cf, ci, ci, vp, cs, vp]
+    lib.rmsnorm_rowmax.restype = ci
     lib.attn_status_string.argtypes = [ci]
     lib.attn_status_string.restype = ctypes.c_char_p
     lib.attn_last_hip_error.argtypes = []
@@ -280,6 +299,92 @@ def attn_decode_kernels(Hq, Hkv, D, dtype, alibi, softcap=0.0):
     _check(load_library().attn_decode_kernels(Hq, Hkv, D, _DTYPE_CODE.get(dtype, dtype), int(bool(alibi)),
                                               float(softcap or 0.0), buf, 256))
     return buf.value.decode().split(";")
+
+
+def peaks_hbm_read(buf, sink=None, stream=None):
+    """Stream-read every byte of the GPU tensor ``buf`` once (peaks.h).  Returns ``sink``."""
+    lib = load_library()
+    if sink is None:
+        sink = torch.empty(lib.peaks_hbm_read_sink_floats(), dtype=torch.float32, device=buf.device)
+    _check(lib.peaks_hbm_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)))
+    return sink
+
+
+def peaks_mfma(dtype, iters, operands, sink=None, clocks=None, stream=None):
+    """Run the MFMA loop of peaks.h; returns (sink, clocks) tensors."""
+    lib = load_library()
+    if sink is None:
+        sink = torch.empty(lib.peaks_mfma_waves(), dtype=torch.float32, device=operands.device)
+    if clocks is None:
+        clocks = torch.zeros(2, dtype=torch.int64, device=operands.device)
+    _check(lib.peaks_mfma(_DTYPE_CODE.get(dtype, dtype), int(iters), _ptr(operands), _ptr(sink), _ptr(clocks),
+                          _stream(stream)))
+    return sink, clocks
+
+
+def peaks_mfma_waves():
+    return load_library().peaks_mfma_waves()
+
+
+def peaks_mfma_operand_bytes():
+    return load_library().peaks_mfma_operand_bytes()
+
+
+NORM_F16, NORM_BF16, NORM_F32 = 0, 1, 2
+_NORM_CODE = {torch.float16: NORM_F16, torch.bfloat16: NORM_BF16, torch.float32: NORM_F32}
+
+
+def norm_chunks(N, M, dtype):
+    return load_library().norm_chunks(N, M, _NORM_CODE[dtype])
+
+
+def norm_workspace_bytes(N, chunks):
+    return load_library().norm_workspace_bytes(N, chunks)
+
+
+def _norm_args(x, chunks, workspace):
+    _require(x.is_cuda and x.is_contiguous() and x.dim() == 2, "x must be a contiguous 2-D GPU tensor [N, M]")
+    _require(x.dtype in _NORM_CODE, "x must be float16, bfloat16 or float32")
+    N, M = x.shape
+    lib = load_library()
+    C = chunks or lib.norm_chunks(N, M, _NORM_CODE[x.dtype])
+    if workspace is None:
+        workspace = torch.empty(max(lib.norm_workspace_bytes(N, max(C, 1)), 16), dtype=torch.uint8,
+                                device=x.device)
+    return N, M, workspace
+
+
+def norm_l2(x, out=None, *, chunks=0, workspace=None, stream=None):
+    """Row L2 norms of x [N, M] (single pass, split over the row): out [N] float32."""
+    N, M, workspace = _norm_args(x, chunks, workspace)
+    if out is None:
+        out = torch.empty(N, dtype=torch.float32, device=x.device)
+    _require(out.is_cuda and out.dtype == torch.float32 and out.numel() == N, "out must be float32 [N]")
+    _check(load_library().norm_l2(_ptr(x), _ptr(out), N, M, _NORM_CODE[x.dtype], int(chunks), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out
+
+
+def rmsnorm_rowmax(x, y=None, rowmax=None, *, eps=1e-6, chunks=0, workspace=None, stream=None):
+    """y = x / sqrt(mean(x^2) + eps) (x's dtype) and rowmax [N] = max of each row of y (float32)."""
+    N, M, workspace = _norm_args(x, chunks, workspace)
+    if y is None:
+        y = torch.empty_like(x)
+    if rowmax is None:
+        rowmax = torch.empty(N, dtype=torch.float32, device=x.device)
+    _require(y.shape == x.shape and y.dtype == x.dtype and y.is_contiguous() and y.is_cuda, "y must match x")
+    _require(rowmax.is_cuda and rowmax.dtype == torch.float32 and rowmax.numel() == N, "rowmax must be float32 [N]")
+    _check(load_library().rmsnorm_rowmax(_ptr(x), _ptr(y), _ptr(rowmax), N, M, float(eps), _NORM_CODE[x.dtype],
+                                         int(chunks), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                         _stream(stream)))
+    return y, rowmax
+
+
+def norm_partials(workspace, N, chunks):
+    """View a norm workspace as (r [N, chunks], t [N, chunks]) float32."""
+    f = workspace.view(torch.float32)
+    n = N * chunks
+    return f[:n].view(N, chunks), f[n:2 * n].view(N, chunks)
 
 
 def decode_partials(workspace, B, Hq, D, num_splits):

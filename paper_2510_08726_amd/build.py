@@ -44,7 +44,9 @@ DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "
 # canonicalising both inputs first.  The prefill device assembly is kept
 # (-save-temps) for the ISA hazard check in the tests.
 UNITS = [(f"prefill{k}", "prefill.hip", ["-fno-honor-nans", f"-DATTN_PREFILL_SHARD={k}", "-save-temps"])
-         for k in range(4)] + [("decode", "decode.hip", ["-save-temps"]), ("attn_api", "attn_api.cpp", [])]
+         for k in range(4)] + [("decode", "decode.hip", ["-save-temps"]), ("peaks", "peaks.hip", ["-save-temps"]),
+            ("norms", "norms.hip", ["-save-temps"]),
+            ("attn_api", "attn_api.cpp", [])]
 
 
 def unit_dir(name):
@@ -54,7 +56,8 @@ def unit_dir(name):
 
 def device_asm_files():
     """Device assembly of every kernel unit written by the last build()."""
-    return prefill_asm_files() + [os.path.join(unit_dir("decode"), f"decode-hip-amdgcn-amd-amdhsa-{ARCH}.s")]
+    return prefill_asm_files() + [os.path.join(unit_dir(u), f"{u}-hip-amdgcn-amd-amdhsa-{ARCH}.s")
+                                  for u in ("decode", "peaks", "norms")]
 
 
 def prefill_asm_files():

@@ -9,6 +9,8 @@
 #include <limits>
 
 #include "../../include/attn.h"
+#include "../../include/peaks.h"
+#include "../../include/norms.h"
 #include "launch.h"
 
 namespace {
@@ -269,6 +271,84 @@ int attn_decode_kernels(int Hq, int Hkv, int D, attn_dtype dtype, int alibi, flo
     std::snprintf(s, sizeof s, "decode_split_kernel<%d,%s,%d,%d,%d>;decode_combine_kernel<%d,%s>", D,
                   dtype_name(dtype), gh, a, c, D, dtype_name(dtype));
   return put(buf, len, s);
+}
+
+int peaks_hbm_read(const void* buf, size_t bytes, float* sink, hipStream_t stream) {
+  if (!buf || !sink || bytes < 16 || bytes % 16 || (reinterpret_cast<uintptr_t>(buf) & 15)) return ATTN_ERR_SHAPE;
+  const hipError_t e = attn::launch_hbm_read(buf, bytes, sink, stream);
+  return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
+int peaks_hbm_read_sink_floats(void) { return attn::hbm_read_sink_floats(); }
+
+int peaks_mfma(int dtype, int iters, const void* operands, float* sink, unsigned long long* clocks,
+               hipStream_t stream) {
+  if (!operands || !sink || !clocks || iters < 1 || (dtype != 0 && dtype != 1)) return ATTN_ERR_SHAPE;
+  const hipError_t e = attn::launch_mfma_loop(dtype, iters, operands, sink, clocks, stream);
+  return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
+int peaks_mfma_waves(void) { return attn::mfma_loop_waves(); }
+
+size_t peaks_mfma_operand_bytes(void) { return attn::mfma_loop_operand_bytes(); }
+
+int norm_chunks(int N, int M, norm_dtype dtype) {
+  if (N < 1 || M < 1 || (dtype != NORM_F16 && dtype != NORM_BF16 && dtype != NORM_F32)) return 0;
+  constexpr int kTargetBlocks = 2048, kMinChunk = 4096;
+  int64_t c = (kTargetBlocks + N - 1) / N;
+  const int64_t cmax = ((int64_t)M + kMinChunk - 1) / kMinChunk;
+  if (c > cmax) c = cmax;
+  return c < 1 ? 1 : (int)c;
+}
+
+size_t norm_workspace_bytes(int N, int chunks) {
+  if (N < 1 || chunks < 1) return 0;
+  const size_t bytes = (size_t)N * chunks * 2 * sizeof(float);
+  return (bytes + 255) & ~(size_t)255;
+}
+
+}  // extern "C"
+
+namespace {
+
+int norm_run(const void* X, void* Y, float* out, int N, int M, float eps, norm_dtype dtype, int chunks,
+             void* workspace, size_t workspace_bytes, bool rms, hipStream_t stream) {
+  if (!X || !out || !workspace || (rms && !Y)) return ATTN_ERR_NULL;
+  if (dtype != NORM_F16 && dtype != NORM_BF16 && dtype != NORM_F32) return ATTN_ERR_UNSUPPORTED;
+  const int vec = dtype == NORM_F32 ? 4 : 8;
+  if (N < 1 || M < 1 || M % vec || chunks < 0 || !std::isfinite(eps) || eps < 0.f) return ATTN_ERR_SHAPE;
+  if ((int64_t)N * M >= (int64_t(1) << 40)) return ATTN_ERR_SHAPE;
+  const int C = chunks ? chunks : norm_chunks(N, M, dtype);
+  if ((int64_t)N * C > kMaxGrid) return ATTN_ERR_SHAPE;
+  if (workspace_bytes < norm_workspace_bytes(N, C) || (reinterpret_cast<uintptr_t>(workspace) & 15))
+    return ATTN_ERR_WORKSPACE;
+  attn::NormParams p{};
+  p.x = X; p.y = Y; p.out = out;
+  p.ws_r = static_cast<float*>(workspace);
+  p.ws_t = p.ws_r + (size_t)N * C;
+  p.N = N; p.M = M; p.chunks = C;
+  const int64_t per = ((int64_t)M + C - 1) / C;
+  p.chunk = (int)((per + vec - 1) / vec * vec);
+  p.dtype = (int)dtype;
+  p.rms = rms ? 1 : 0;
+  p.eps = eps;
+  p.invM = 1.f / (float)M;
+  const hipError_t e = attn::launch_norm(p, stream);
+  return e == hipSuccess ? ATTN_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int norm_l2(const void* X, float* out, int N, int M, norm_dtype dtype, int chunks,
+            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return norm_run(X, nullptr, out, N, M, 0.f, dtype, chunks, workspace, workspace_bytes, false, stream);
+}
+
+int rmsnorm_rowmax(const void* X, void* Y, float* rowmax, int N, int M, float eps, norm_dtype dtype,
+                   int chunks, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return norm_run(X, Y, rowmax, N, M, eps, dtype, chunks, workspace, workspace_bytes, true, stream);
 }
 
 }  // extern "C"

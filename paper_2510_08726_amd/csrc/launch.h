@@ -83,4 +83,29 @@ constexpr size_t kDecodeScratchBytes = size_t(16) << 20;
 // device, then cached).
 hipError_t decode_scratch(void** ptr);
 
+// Row reductions (norms.hip): the stable L2 norm, or RMSNorm with its row max.
+struct NormParams {
+  const void* x;
+  void* y;              // RMSNorm output [N, M], or nullptr
+  float* out;           // [N]: the norms, or the row maxima of y
+  float* ws_r;          // [N * chunks] partials r
+  float* ws_t;          // [N * chunks] partials t
+  int N, M;
+  int chunks;           // chunks per row
+  int chunk;            // elements per chunk (whole 16-byte vectors)
+  int dtype;            // 0 fp16, 1 bf16, 2 fp32
+  int rms;              // 1: RMSNorm with row max, 0: L2 norm
+  float eps;
+  float invM;           // 1 / M
+};
+hipError_t launch_norm(const NormParams& p, hipStream_t stream);
+
+// Achievable-peak probes (peaks.hip).
+hipError_t launch_hbm_read(const void* buf, size_t bytes, float* sink, hipStream_t stream);
+int hbm_read_sink_floats();
+hipError_t launch_mfma_loop(int bf16, int iters, const void* operands, float* sink, unsigned long long* clocks,
+                            hipStream_t stream);
+int mfma_loop_waves();
+size_t mfma_loop_operand_bytes();
+
 }  // namespace attn

@@ -1,0 +1,274 @@
+// Row reductions fused by rolling update and split by split-k update: the
+// stable L2 norm and RMSNorm with the row max of its output (the paper's
+// second workload; see include/norms.h).  Both are HBM streams: every lane
+// reads 16-byte vectors of its row chunk, folds each vector into its state
+// with one repaired update (the vector's own max and sum first, the
+// privatised local reduction), the 256 lanes' states are combined with the
+// same repair, and the chunk partials of a row are combined by the second
+// kernel.
+
+#include <type_traits>
+
+#include "kernel_common.h"
+#include "launch.h"
+
+namespace attn {
+
+namespace {
+
+constexpr int kNormThreads = 256;
+constexpr int kNormUnroll = 4;   // 16-byte loads in flight per lane
+
+template <typename T> struct Vec;
+template <> struct Vec<_Float16> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void load(const u32x4& w, float* f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t u = w[i];   // (a bit_cast of the element itself reads element 0 on this compiler)
+      const f16x2 h = __builtin_bit_cast(f16x2, u);
+      f[2 * i] = (float)h[0];
+      f[2 * i + 1] = (float)h[1];
+    }
+  }
+  static __device__ __forceinline__ u32x4 store(const float* f) {
+    u32x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = Elem<_Float16>::pack2(f[2 * i], f[2 * i + 1]);
+    return w;
+  }
+};
+template <> struct Vec<__bf16> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void load(const u32x4& w, float* f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = Elem<__bf16>::lo(w[i]);
+      f[2 * i + 1] = Elem<__bf16>::hi(w[i]);
+    }
+  }
+  static __device__ __forceinline__ u32x4 store(const float* f) {
+    u32x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = Elem<__bf16>::pack2(f[2 * i], f[2 * i + 1]);
+    return w;
+  }
+};
+template <> struct Vec<float> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void load(const u32x4& w, float* f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t u = w[i];   // as above
+      f[i] = __builtin_bit_cast(float, u);
+    }
+  }
+  static __device__ __forceinline__ u32x4 store(const float* f) {
+    u32x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float x = f[i];
+      w[i] = __builtin_bit_cast(uint32_t, x);
+    }
+    return w;
+  }
+};
+
+// The rolling state of one lane and its two updates: fold one vector of VN
+// values (privatised: the vector's own reduction, then one repaired global
+// update), and merge another state (the split-k combine of two partials).
+//
+// L2: r = max |x| so far, t = sum of (x / r)^2 so far.
+struct L2State {
+  float r = 0.f, t = 0.f;
+  template <int VN>
+  __device__ __forceinline__ void fold(const float* c, float, float) {
+    float vm = 0.f;
+#pragma unroll
+    for (int k = 0; k < VN; ++k) vm = fmaxf(vm, fabsf(c[k]));
+    const float rn = fmaxf(r, vm);
+    if (rn > 0.f) {                                    // uniform over real data; zeros change nothing
+      const float inv = 1.f / rn;
+      const float a = r * inv;                         // h: t (r / r')^2
+      float tn = t * a * a;
+#pragma unroll
+      for (int k = 0; k < VN; ++k) {
+        const float q = c[k] * inv;                    // g(r', c) = (c / r')^2
+        tn = __builtin_fmaf(q, q, tn);
+      }
+      t = tn;
+      r = rn;
+    }
+  }
+  __device__ __forceinline__ void merge(float r2, float t2, float) {
+    const float rn = fmaxf(r, r2);
+    if (rn > 0.f) {
+      const float a = r / rn, b = r2 / rn;
+      t = t * a * a + t2 * b * b;
+      r = rn;
+    }
+  }
+};
+
+// RMSNorm statistics: r = sum of x^2 / M so far (the running mean), t = max
+// of x / sqrt(r + eps) so far.
+struct RmsState {
+  float r = 0.f, t = kNegInf;
+  template <int VN>
+  __device__ __forceinline__ void fold(const float* c, float invM, float eps) {
+    float s = 0.f, vm = kNegInf;
+#pragma unroll
+    for (int k = 0; k < VN; ++k) {
+      s = __builtin_fmaf(c[k], c[k], s);
+      vm = fmaxf(vm, c[k]);
+    }
+    const float rn = __builtin_fmaf(s, invM, r);
+    const float q = __builtin_amdgcn_rsqf(rn + eps);   // 1 / sqrt(r' + eps)
+    // h(t, r, r') = t sqrt(r + eps) / sqrt(r' + eps); g(r', c) = c / sqrt(r' + eps).
+    // Before the first value t is -inf and stays so under h (also when
+    // r + eps = 0, where the factor would be 0).
+    t = fmaxf(repair(t, r, q, eps), vm * q);
+    r = rn;
+  }
+  __device__ __forceinline__ void merge(float r2, float t2, float eps) {
+    const float rn = r + r2;
+    const float q = __builtin_amdgcn_rsqf(rn + eps);
+    t = fmaxf(repair(t, r, q, eps), repair(t2, r2, q, eps));
+    r = rn;
+  }
+  // h(t, r, r') with q = 1 / sqrt(r' + eps).
+  static __device__ __forceinline__ float repair(float t, float r, float q, float eps) {
+    return t == kNegInf ? kNegInf : t * (__builtin_sqrtf(r + eps) * q);
+  }
+};
+
+template <typename T, typename S>
+__device__ __forceinline__ void fold_chunk(const NormParams& p, int n, int c, S& st) {
+  constexpr int VN = Vec<T>::N;
+  // This chunk's vectors.
+  const int v0 = (int)(min((long long)c * p.chunk, (long long)p.M) / VN);
+  const int v1 = (int)(min((long long)(c + 1) * p.chunk, (long long)p.M) / VN);
+  const u32x4* row = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.x) + (size_t)n * p.M);
+  int v = v0 + threadIdx.x;
+  for (; v + (kNormUnroll - 1) * kNormThreads < v1; v += kNormUnroll * kNormThreads) {
+    u32x4 w[kNormUnroll];
+#pragma unroll
+    for (int u = 0; u < kNormUnroll; ++u) w[u] = row[v + u * kNormThreads];
+#pragma unroll
+    for (int u = 0; u < kNormUnroll; ++u) {
+      float f[VN];
+      Vec<T>::load(w[u], f);
+      st.template fold<VN>(f, p.invM, p.eps);
+    }
+  }
+  for (; v < v1; v += kNormThreads) {
+    float f[VN];
+    Vec<T>::load(row[v], f);
+    st.template fold<VN>(f, p.invM, p.eps);
+  }
+}
+
+// Combine the states of the workgroup's 256 lanes (the same repaired merge),
+// leaving the result in lane 0 of wave 0.
+template <typename S>
+__device__ __forceinline__ void block_merge(S& st, float eps) {
+  __shared__ float sr[kNormThreads / 64], stt[kNormThreads / 64];
+#pragma unroll
+  for (int x = 32; x >= 1; x >>= 1) {
+    const float r2 = __shfl_xor(st.r, x, 64), t2 = __shfl_xor(st.t, x, 64);
+    st.merge(r2, t2, eps);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sr[threadIdx.x >> 6] = st.r;
+    stt[threadIdx.x >> 6] = st.t;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int w = 1; w < kNormThreads / 64; ++w) st.merge(sr[w], stt[w], eps);
+  }
+}
+
+// Local nests: one workgroup per (chunk c, row n) writes its partial (r, t).
+template <typename T, bool RMS>
+__global__ __launch_bounds__(kNormThreads) void norm_split_kernel(NormParams p) {
+  const int c = blockIdx.x % p.chunks, n = blockIdx.x / p.chunks;
+  typename std::conditional<RMS, RmsState, L2State>::type st;
+  fold_chunk<T>(p, n, c, st);
+  block_merge(st, p.eps);
+  if (threadIdx.x == 0) {
+    p.ws_r[blockIdx.x] = st.r;
+    p.ws_t[blockIdx.x] = st.t;
+  }
+}
+
+// Global nest of the L2 norm: one thread per row combines its chunks.
+__global__ __launch_bounds__(kNormThreads) void l2_combine_kernel(NormParams p) {
+  const int n = blockIdx.x * kNormThreads + threadIdx.x;
+  if (n >= p.N) return;
+  L2State st;
+  for (int c = 0; c < p.chunks; ++c) st.merge(p.ws_r[n * p.chunks + c], p.ws_t[n * p.chunks + c], 0.f);
+  p.out[n] = st.r * __builtin_sqrtf(st.t);
+}
+
+// RMSNorm output: every workgroup (chunk c, row n) combines its row's
+// partials (s = the row mean of x^2, m = the row max of y), writes m if it
+// holds chunk 0, and writes its chunk of y = x / sqrt(s + eps).
+template <typename T>
+__global__ __launch_bounds__(kNormThreads) void rms_apply_kernel(NormParams p) {
+  constexpr int VN = Vec<T>::N;
+  const int c = blockIdx.x % p.chunks, n = blockIdx.x / p.chunks;
+  __shared__ float s_q;
+  if (threadIdx.x < 64) {
+    RmsState st;
+    for (int k = threadIdx.x; k < p.chunks; k += 64) st.merge(p.ws_r[n * p.chunks + k], p.ws_t[n * p.chunks + k], p.eps);
+#pragma unroll
+    for (int x = 32; x >= 1; x >>= 1) {
+      const float r2 = __shfl_xor(st.r, x, 64), t2 = __shfl_xor(st.t, x, 64);
+      st.merge(r2, t2, p.eps);
+    }
+    if (threadIdx.x == 0) {
+      s_q = 1.f / __builtin_sqrtf(st.r + p.eps);
+      if (c == 0) p.out[n] = st.t;
+    }
+  }
+  __syncthreads();
+  const float q = s_q;
+  const int v0 = (int)(min((long long)c * p.chunk, (long long)p.M) / VN);
+  const int v1 = (int)(min((long long)(c + 1) * p.chunk, (long long)p.M) / VN);
+  const u32x4* row = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.x) + (size_t)n * p.M);
+  u32x4* yrow = reinterpret_cast<u32x4*>(reinterpret_cast<T*>(p.y) + (size_t)n * p.M);
+  for (int v = v0 + threadIdx.x; v < v1; v += kNormThreads) {
+    float f[VN];
+    Vec<T>::load(row[v], f);
+#pragma unroll
+    for (int k = 0; k < VN; ++k) f[k] *= q;
+    yrow[v] = Vec<T>::store(f);
+  }
+}
+
+template <typename T>
+hipError_t launch_norm_t(const NormParams& p, hipStream_t stream) {
+  const dim3 grid(p.N * p.chunks), block(kNormThreads);
+  if (p.rms) {
+    hipLaunchKernelGGL((norm_split_kernel<T, true>), grid, block, 0, stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((rms_apply_kernel<T>), grid, block, 0, stream, p);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((norm_split_kernel<T, false>), grid, block, 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(l2_combine_kernel, dim3((p.N + kNormThreads - 1) / kNormThreads), block, 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_norm(const NormParams& p, hipStream_t stream) {
+  if (p.dtype == 2) return launch_norm_t<float>(p, stream);
+  return p.dtype == 1 ? launch_norm_t<__bf16>(p, stream) : launch_norm_t<_Float16>(p, stream);
+}
+
+}  // namespace attn

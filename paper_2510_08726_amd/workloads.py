@@ -76,6 +76,41 @@ WORKLOADS = {
 }
 
 
+@dataclass(frozen=True)
+class NormWorkload:
+    """A row reduction of the paper's second workload: X [N, M] of dtype."""
+    name: str
+    op: str          # "l2" (stable L2 norm) or "rms" (RMSNorm with the row max of y)
+    N: int
+    M: int
+    dtype: str
+    seed: int
+    eps: float = 1e-6
+
+
+# The largest shape of the paper's range (N 32..256 rows, M 2^10..2^17
+# columns): the L2 norm on fp32 rows (where squares of large entries overflow
+# and the stable form matters), RMSNorm on bf16 activations.
+NORM_DTYPES = {"f16": torch.float16, "bf16": torch.bfloat16, "f32": torch.float32}
+NORM_WORKLOADS = {
+    "l2_norm": NormWorkload("l2_norm", "l2", 256, 1 << 17, "f32", seed=11),
+    "rmsnorm_rowmax": NormWorkload("rmsnorm_rowmax", "rms", 256, 1 << 17, "bf16", seed=12),
+}
+
+
+def make_norm_input(w: NormWorkload, *, seed=None, device="cpu"):
+    """X [N, M]: iid N(0, 1) drawn in float32 from PCG64(seed), rounded once to w.dtype."""
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    x = torch.from_numpy(rng.standard_normal(size=(w.N, w.M), dtype=np.float32)).to(NORM_DTYPES[w.dtype])
+    return x.to(device) if device != "cpu" else x
+
+
+def norm_bytes(op, N, M, elem):
+    """Algorithmic HBM bytes of one call: X read once, the [N] fp32 outputs,
+    and for RMSNorm the output Y."""
+    return N * M * elem * (2 if op == "rms" else 1) + 4 * N
+
+
 def alibi_slopes(H):
     """ALiBi slopes 2^(-8 h / H) for heads h = 1..H, as float32 (one per head).
 

@@ -27,15 +27,20 @@ def lib():
 
 
 def declared_functions():
-    src = open(os.path.join(ROOT, "include", "attn.h")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(attn_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names.update(re.findall(r"\b((?:attn|peaks|norm)_[a-z0-9_]+|rmsnorm_rowmax)\s*\(", src))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
     assert {"attn_fwd", "attn_fwd_mod", "attn_decode", "attn_decode_mod", "attn_decode_workspace_bytes",
             "attn_decode_num_splits", "attn_status_string", "attn_last_hip_error"} <= set(names)
+    assert {"peaks_hbm_read", "peaks_mfma", "attn_decode_noalloc", "norm_l2", "rmsnorm_rowmax",
+            "norm_chunks", "norm_workspace_bytes"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
 
