@@ -11,7 +11,7 @@ function attribute "amdgpu-agpr-alloc" sets the AGPR share instead, but has
 no source-level spelling.  So the prefill units run hipcc's own compile steps
 (as printed by `hipcc -###`) and set the attribute on every kernel in the
 device IR between the front end and the back end, which leaves the kernels
-256 - 104 = 152 VGPRs.
+256 - 104 = 152 VGPRs at D = 128 and 256 - 56 = 200 at D = 64.
 """
 
 import os
@@ -30,9 +30,10 @@ LIB = os.path.join(PKG, "libattn.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 LLVM_DIS = "/opt/rocm/llvm/bin/llvm-dis"
-# AGPRs reserved for the prefill kernels' fixed operands (a0..a101), in the
-# allocation granularity of 4.
-PREFILL_AGPRS = 104
+# AGPRs reserved for the prefill kernels' fixed operands, in the allocation
+# granularity of 4, per shard: D = 128 (shards 0, 1) uses a0..a101, D = 64
+# (shards 2, 3) a0..a53.
+PREFILL_AGPRS = {0: 104, 1: 104, 2: 56, 3: 56}
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++20", "-fPIC", "-I", INCLUDE, "-I", CSRC]
 DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -120,7 +121,7 @@ def build(verbose=False):
     def run(job):
         name, src, cmd = job
         if src == "prefill.hip":
-            return compile_with_agprs(cmd, unit_dir(name), PREFILL_AGPRS)
+            return compile_with_agprs(cmd, unit_dir(name), PREFILL_AGPRS[int(name[len("prefill"):])])
         p = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True, cwd=unit_dir(name))
         return p.returncode, p.stdout
 

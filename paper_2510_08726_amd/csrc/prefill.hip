@@ -125,23 +125,42 @@ __device__ __forceinline__ void hazard_pad() {
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
 
+// This file is compiled once per (head dim, element type) shard, selected by
+// ATTN_PREFILL_SHARD (0, 1: D = 128; 2, 3: D = 64), so the instantiations
+// build in parallel and each shard gets the register split of its head dim.
+#ifndef ATTN_PREFILL_SHARD
+#define ATTN_PREFILL_SHARD 0
+#endif
+constexpr int kShardD = ATTN_PREFILL_SHARD >= 2 ? 64 : 128;
+
 // Register files.  The S^T accumulators, P and the LDS operands are ordinary
 // values in VGPRs, allocated by the compiler.  The operands that live through
 // the whole key loop are in fixed AGPRs that only the inline assembly below
-// names: O^T block db in a[16 db .. + 15] (64 for D = 128), Q fragment kx in
-// a[64 + 4 kx .. + 3], l in a[96 .. 99], the ones in a[100 .. 101].  So 102
-// AGPRs, which leaves 152 VGPRs of a wave's 256 at two waves per SIMD.
-// Every statement that touches them lists all of them as clobbered, so the
-// compiler keeps none of its own values there, and counts them as used.
+// names: O^T block db in a[16 db .. + 15] (D / 2 registers), Q fragment kx in
+// a[kQAgpr + 4 kx .. + 3] (D / 4), l in a[kLAgpr .. + 3], the ones in
+// a[kOnesAgpr .. + 1]: 102 AGPRs for D = 128, 54 for D = 64.  The build sets
+// each kernel's AGPR allocation to that count rounded up to 4 (104 or 56),
+// which leaves 152 or 200 of a wave's 256 registers (two waves per SIMD) to
+// the VGPRs.  Every statement that touches the fixed AGPRs lists all of them
+// as clobbered, so the compiler keeps none of its own values there, and
+// counts them as used.
 #define ATTN_A10(p) "a" #p "0", "a" #p "1", "a" #p "2", "a" #p "3", "a" #p "4", \
                     "a" #p "5", "a" #p "6", "a" #p "7", "a" #p "8", "a" #p "9"
+#if ATTN_PREFILL_SHARD >= 2
+#define ATTN_AGPRS "a0", "a1", "a2", "a3", "a4", "a5", "a6", "a7", "a8", "a9", \
+    ATTN_A10(1), ATTN_A10(2), ATTN_A10(3), ATTN_A10(4), "a50", "a51", "a52", "a53"
+#else
 #define ATTN_AGPRS "a0", "a1", "a2", "a3", "a4", "a5", "a6", "a7", "a8", "a9", \
     ATTN_A10(1), ATTN_A10(2), ATTN_A10(3), ATTN_A10(4), ATTN_A10(5), ATTN_A10(6), ATTN_A10(7), ATTN_A10(8), ATTN_A10(9), \
     "a100", "a101"
+#endif
 constexpr int kOAgpr = 0;
-constexpr int kQAgpr = 64;
-constexpr int kLAgpr = 96;      // exp-sum accumulator
-constexpr int kOnesAgpr = 100;  // two registers holding (1.0, 1.0)
+constexpr int kQAgpr = kOAgpr + kShardD / 2;
+constexpr int kLAgpr = kQAgpr + kShardD / 4;    // exp-sum accumulator
+constexpr int kOnesAgpr = kLAgpr + 4;           // two registers holding (1.0, 1.0)
+constexpr int kAgprAlloc = (kOnesAgpr + 2 + 3) / 4 * 4;
+constexpr int kVgprBudget = 256 - kAgprAlloc;
+static_assert(kOnesAgpr + 2 == (kShardD == 64 ? 54 : 102), "the clobber list names every fixed AGPR");
 
 // 32x32x16 MFMAs.  qk0/qk: S^T accumulator in VGPRs (qk0 starts from zero), K
 // operand in VGPRs, Q operand from AGPRs a[QA .. QA + 3]; with PAD, two wait
@@ -150,7 +169,8 @@ constexpr int kOnesAgpr = 100;  // two registers holding (1.0, 1.0)
 // all-ones operand, which adds the four 16-bit values each lane holds in b to
 // every register of its accumulator a[LA .. LA + 3]: the exp-sum l is
 // accumulated from the same rounded weights that multiply V, on the matrix
-// unit.  (Its s_nop 1 covers a VALU write of b just before it.)
+// unit.  Its b was packed an iteration earlier; the wait-state check of the
+// generated code confirms that no VALU write of b comes within two states.
 template <typename T> struct Mma;
 template <> struct Mma<_Float16> {
   typedef f16x8 v8;
@@ -171,7 +191,7 @@ template <> struct Mma<_Float16> {
   }
   static constexpr uint32_t kOnes = 0x3c003c00u;   // (1.0, 1.0)
   template <int LA> static __device__ __forceinline__ void rowsum(uint2 b) {
-    asm volatile("s_nop 1\n\tv_mfma_f32_4x4x4_16b_f16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
+    asm volatile("v_mfma_f32_4x4x4_16b_f16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
                  : : "v"(b), "n"(LA), "n"(LA + 3), "n"(kOnesAgpr), "n"(kOnesAgpr + 1) : ATTN_AGPRS);
   }
 };
@@ -194,7 +214,7 @@ template <> struct Mma<__bf16> {
   }
   static constexpr uint32_t kOnes = 0x3f803f80u;   // (1.0, 1.0)
   template <int LA> static __device__ __forceinline__ void rowsum(uint2 b) {
-    asm volatile("s_nop 1\n\tv_mfma_f32_4x4x4_16b_bf16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
+    asm volatile("v_mfma_f32_4x4x4_16b_bf16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
                  : : "v"(b), "n"(LA), "n"(LA + 3), "n"(kOnesAgpr), "n"(kOnesAgpr + 1) : ATTN_AGPRS);
   }
 };
@@ -279,11 +299,12 @@ struct Prefill {
   static_assert(NG == 2 * DB, "as many V fragments as K fragments");
   static_assert(CPW >= 1 && 2 * NB == CPW * kWaves, "the copies of a tile divide evenly over the waves");
   // K and V operand fragments read ahead of their MFMA (one K fragment is two
-  // MFMA slots).  With ALiBi (keys visited last to first, more live state)
-  // the V ring is shallower too.  Deeper K rings measured slower: the
-  // registers they hold push the per-item code into scratch.
-  static constexpr int PFD_K = 1;
-  static constexpr int PFD_V = LOG2 ? 1 : 3;
+  // MFMA slots).  At D = 128 the VGPR budget allows one K fragment ahead and,
+  // with ALiBi or SoftCap (more live state), one V fragment; deeper rings
+  // push the per-item code into scratch.  At D = 64 the smaller AGPR share
+  // leaves room for three of each.
+  static constexpr int PFD_K = D == 64 ? 3 : 1;
+  static constexpr int PFD_V = (LOG2 || WIN) ? 1 : 3;
   template <bool IS_K> static constexpr int pfd() { return IS_K ? PFD_K : PFD_V; }
   static_assert(NG % (PFD_K + 1) == 0 && NG % (PFD_V + 1) == 0, "fragment ring positions must repeat every iteration");
   static_assert(kOAgpr + 16 * DB <= kQAgpr && kQAgpr + 4 * KX <= kLAgpr, "AGPR map");
@@ -508,6 +529,12 @@ struct Prefill {
     constexpr bool MASKED = SM == 2;
     constexpr bool PREP = LOG2 || MASKED;
     typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
+    // Every softmax step of the tile runs inside these NS slots, before the
+    // lazy-rescale check reads the lane maximum and before the next
+    // iteration's P.V reads the packed weights: a step left past the last
+    // slot would leave P words unwritten (uninitialised registers on the
+    // first tiles of an item) and the lane maximum incomplete.
+    static_assert(P::begin(0, NS) == 0 && P::begin(NS, NS) == P::NSTEP, "the steps cover the tile within the slots");
     [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
       (
           [&] {
@@ -562,11 +589,13 @@ struct Prefill {
 };
 
 // Two waves per SIMD (two workgroups per compute unit) leave each wave 256
-// registers: the 102 AGPRs named by the inline assembly and at most 152
-// VGPRs.  (By itself the compiler would halve the file once AGPRs are used;
-// the build sets the kernels' AGPR allocation to 104 in the device IR.)
+// registers: the fixed AGPRs named by the inline assembly and at most
+// kVgprBudget VGPRs.  (By itself the compiler would halve the file once AGPRs
+// are used; the build sets the kernels' AGPR allocation to kAgprAlloc in the
+// device IR.)
 template <int D, typename T, bool CAUSAL, bool ALIBI, bool CAP, bool WIN>
-__global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(152))) void prefill_kernel(PrefillParams p) {
+__global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(kVgprBudget))) void prefill_kernel(PrefillParams p) {
+  static_assert(D == kShardD, "one head dim per shard");
   typedef Prefill<D, T, CAUSAL, ALIBI, CAP, WIN> PF;
   constexpr bool REV = ALIBI;
   typedef typename PF::State State;
@@ -1011,12 +1040,7 @@ hipError_t launch_d(const PrefillParams& p, hipStream_t s) {
 
 }  // namespace
 
-// This file is compiled once per (head dim, element type) shard, selected by
-// ATTN_PREFILL_SHARD, so the instantiations build in parallel; shard 0 also
-// holds the dispatcher.
-#ifndef ATTN_PREFILL_SHARD
-#define ATTN_PREFILL_SHARD 0
-#endif
+// Shard 0 also holds the dispatcher.
 #if ATTN_PREFILL_SHARD == 0
 hipError_t launch_prefill_d128_f16(const PrefillParams& p, hipStream_t s) { return launch_d<128, _Float16>(p, s); }
 #elif ATTN_PREFILL_SHARD == 1
