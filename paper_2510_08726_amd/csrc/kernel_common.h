@@ -69,11 +69,13 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // SoftCap of a score in log2 units (x = s log2 e): cap tanh(s / cap) log2 e,
 // from tanh(y) = 1 - 2 / (1 + e^{2y}) with e^{2y} = 2^(x k2); k2 = 2 / cap,
 // cl = cap log2 e.  The exponential saturates to inf or 0 for large |x|, which
-// gives +-cl exactly.
-__device__ __forceinline__ float soft_cap(float x, float k2, float cl) {
+// gives +-cl exactly.  `add` replaces the final + cl (cl minus an offset
+// folds that offset into the same instruction).
+__device__ __forceinline__ float soft_cap(float x, float k2, float cl, float add) {
   const float e = fast_exp2(x * k2);
-  return __builtin_fmaf(-2.f * cl, __builtin_amdgcn_rcpf(1.f + e), cl);
+  return __builtin_fmaf(-2.f * cl, __builtin_amdgcn_rcpf(1.f + e), add);
 }
+__device__ __forceinline__ float soft_cap(float x, float k2, float cl) { return soft_cap(x, k2, cl, cl); }
 
 // K and V tiles live in LDS row-major, [keys][D], with the 16-byte chunks of
 // each row XOR-swizzled: chunk c of row r sits at chunk position c ^ swz(r).

@@ -333,6 +333,7 @@ struct Prefill {
     float k2, cl; // SoftCap: 2 / cap and cap * log2(e)
     float sl2;    // ALiBi slope * log2(e)
     float abase;  // ALiBi bias of key j0 + 4 hh relative to the wave's first row
+    float mb;     // (ALiBi bias base, or SoftCap cl) minus the row's reference max
     int lim;      // last visible key offset (key - j0 - 4 hh) of this lane's row
     int llo;      // first visible key offset of this lane's row (sliding window)
     float t;      // this lane's maximum score of the tile
@@ -411,17 +412,25 @@ struct Prefill {
   // is dropped: it shifts a whole row by a constant, which the row's softmax
   // does not see.  Masked tiles set keys past Lk and (causal) keys after the
   // row to -inf before the max.
-  template <int K, bool PREP, bool MASKED>
+  //
+  // REL (whole tiles of ALiBi or SoftCap kernels after a wave's first tile,
+  // when every row has a finite reference): the reference max is folded into
+  // the additive term of the bias or cap, so the prepared value is already
+  // the exponent, s c + bias - m (or the capped score - m), and the maximum
+  // and the lazy check work relative to m.
+  template <int K, bool PREP, bool MASKED, bool REL>
   static __device__ __forceinline__ void soft_step(State& st, Scores& sc, Probs& pr, TileArgs& ta) {
     typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
     const float ce = LOG2 ? 1.f : ta.c;
+    static_assert(!REL || (LOG2 && !MASKED), "the relative form is for whole tiles with a bias or cap");
     if constexpr (K < P::MAX0) {
       constexpr int r0 = 4 * K;
       // Registers r0 .. r0 + 3 hold keys kconst(r0) + 0..3: their biases are
       // the bias of the first plus 0..3 slopes.
       [[maybe_unused]] float b[4] = {0.f, 0.f, 0.f, 0.f};
       if constexpr (ALIBI) {
-        b[0] = r0 == 0 ? ta.abase : __builtin_fmaf(ta.sl2, (float)kconst(r0), ta.abase);
+        const float base = REL ? ta.mb : ta.abase;
+        b[0] = r0 == 0 ? base : __builtin_fmaf(ta.sl2, (float)kconst(r0), base);
         b[1] = b[0] + ta.sl2;
         b[2] = __builtin_fmaf(ta.sl2, 2.f, b[0]);
         b[3] = __builtin_fmaf(ta.sl2, 2.f, b[1]);
@@ -429,7 +438,7 @@ struct Prefill {
 #pragma unroll
       for (int r = r0; r < r0 + 4; ++r) {
         if constexpr (CAP) {
-          const float x = soft_cap(sc[r] * ta.c, ta.k2, ta.cl);
+          const float x = soft_cap(sc[r] * ta.c, ta.k2, ta.cl, REL && !ALIBI ? ta.mb : ta.cl);
           sc[r] = ALIBI ? x + b[r - r0] : x;
         } else if constexpr (ALIBI) {
           sc[r] = __builtin_fmaf(sc[r], ta.c, b[r - r0]);
@@ -443,8 +452,8 @@ struct Prefill {
       }
     } else if constexpr (P::is_exp(K)) {
       constexpr int r = 2 * P::exp_index(K);
-      const float p0 = fast_exp2(__builtin_fmaf(sc[r], ce, -st.mc));
-      const float p1 = fast_exp2(__builtin_fmaf(sc[r + 1], ce, -st.mc));
+      const float p0 = fast_exp2(REL ? sc[r] : __builtin_fmaf(sc[r], ce, -st.mc));
+      const float p1 = fast_exp2(REL ? sc[r + 1] : __builtin_fmaf(sc[r + 1], ce, -st.mc));
       uint32_t w = E::pack2(p0, p1);
       pin(w);
       pr.w[r / 8][(r % 8) / 2] = w;
@@ -460,9 +469,10 @@ struct Prefill {
   // After the steps of a tile: does some score of this lane exceed the
   // reference maximum by more than the lazy threshold?  (Then the tile's P,
   // computed against the old reference, must be recomputed: see resolve.)
+  template <bool REL>
   static __device__ __forceinline__ bool exceeds(const State& st, const TileArgs& ta) {
     const float ce = LOG2 ? 1.f : ta.c;
-    return __builtin_fmaf(ta.t, ce, -st.mc) > kLazyThreshold;
+    return (REL ? ta.t : __builtin_fmaf(ta.t, ce, -st.mc)) > kLazyThreshold;
   }
 
   // Slow path of a tile whose maximum moved past the threshold in some row
@@ -473,25 +483,35 @@ struct Prefill {
   // tile's products are added (the products so far used the old reference),
   // and the tile's P is recomputed.  Rows that did not move keep their
   // reference and factor 1.
+  template <bool REL>
   static __device__ __forceinline__ void resolve(State& st, Scores& sc, Probs& pr, TileArgs& ta) {
     typedef SoftPlan<false, false, ALIBI, CAP> P;
     const float ce = LOG2 ? 1.f : ta.c;
     const float tm = max_halves(ta.t);
-    const float d = __builtin_fmaf(tm, ce, -st.mc);
+    const float d = REL ? tm : __builtin_fmaf(tm, ce, -st.mc);
     const bool move = d > kLazyThreshold;
     st.alpha = move ? fast_exp2(-d) : 1.f;
-    st.mc = move ? tm * ce : st.mc;
+    if constexpr (REL) {
+      // The prepared values are relative to the old reference: shift them to
+      // the new one, then recompute the tile's weights.
+      const float dd = move ? d : 0.f;
+      st.mc += dd;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[r] -= dd;
+    } else {
+      st.mc = move ? tm * ce : st.mc;
+    }
     static_for<P::NSTEP>([&](auto kc) {
       constexpr int K = decltype(kc)::value;
-      if constexpr (P::is_exp(K)) soft_step<K, false, false>(st, sc, pr, ta);
+      if constexpr (P::is_exp(K)) soft_step<K, false, false, REL>(st, sc, pr, ta);
     });
   }
 
-  template <int B0, int B1, bool PREP, bool MASKED>
+  template <int B0, int B1, bool PREP, bool MASKED, bool REL>
   static __device__ __forceinline__ void soft_range(State& st, Scores& sc, Probs& pr, TileArgs& ta) {
     if constexpr (B1 > B0) {
       [&]<int... Ks>(std::integer_sequence<int, Ks...>) {
-        (soft_step<B0 + Ks, PREP, MASKED>(st, sc, pr, ta), ...);
+        (soft_step<B0 + Ks, PREP, MASKED, REL>(st, sc, pr, ta), ...);
       }(std::make_integer_sequence<int, B1 - B0>{});
     }
   }
@@ -515,6 +535,12 @@ struct Prefill {
     static_for<pfd<IS_K>()>([&](auto ic) { read_frag<IS_K, decltype(ic)::value>(fr, tile, ad); });
   }
 
+  // Whole tiles after a wave's first one (SM 1 with P.V) take the relative
+  // form in kernels with a bias or cap: every row of the wave has seen a key
+  // by then (its own causal diagonal, or the whole first tile), so its
+  // reference is finite.
+  static constexpr bool rel(int SM, bool PV) { return LOG2 && SM == 1 && PV; }
+
   // The 2 NG MFMA slots of one iteration.  Slot 2 i: S^T MFMA with K fragment
   // i of tile j+1 (kl; QK), slot 2 i + 1: P.V MFMA with V fragment i of tile
   // j-1 (vl; PV) and P(j-1) (pp), plus the row-sum MFMAs of the same
@@ -528,6 +554,7 @@ struct Prefill {
                                                TileArgs& ta, CP&& copy) {
     constexpr bool MASKED = SM == 2;
     constexpr bool PREP = LOG2 || MASKED;
+    constexpr bool REL = rel(SM, PV);
     typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
     // Every softmax step of the tile runs inside these NS slots, before the
     // lazy-rescale check reads the lane maximum and before the next
@@ -568,7 +595,7 @@ struct Prefill {
                   M::template rowsum<kLAgpr>(make_uint2(p_prev.w[c16][2 * db], p_prev.w[c16][2 * db + 1]));
               }
             }
-            if constexpr (SM != 0) soft_range<P::begin(S, NS), P::begin(S + 1, NS), PREP, MASKED>(st, s_cur, p_cur, ta);
+            if constexpr (SM != 0) soft_range<P::begin(S, NS), P::begin(S + 1, NS), PREP, MASKED, REL>(st, s_cur, p_cur, ta);
             __builtin_amdgcn_sched_barrier(0);
           }(),
           ...);
@@ -842,6 +869,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
       if (CAUSAL) l = min(l, row + off - j0 - 4 * hh);
       ta.lim = l;
       if (WIN) ta.llo = row + off + 1 - W - j0 - 4 * hh;
+      if (ALIBI) ta.mb = ta.abase - st.mc;
+      else if (CAP) ta.mb = ta.cl - st.mc;
     };
     // The first iteration with a softmax: O^T and l are still zero there, so
     // its rescale is skipped.
@@ -882,8 +911,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
       PF::template slots<QK, SM, PV>(st, sc[par], sc[par ^ 1], pr[par], pr[par ^ 1], fk, fv, kl_use, kl_nxt,
                                      vl_use, vl_nxt, ad, ta, [&](auto uc) { copy(j, slotc, uc); });
       if constexpr (SM != 0) {
-        if (__builtin_amdgcn_ballot_w64(PF::exceeds(st, ta)) != 0) {
-          PF::resolve(st, sc[par], pr[par], ta);
+        constexpr bool REL = PF::rel(SM, PV);
+        if (__builtin_amdgcn_ballot_w64(PF::template exceeds<REL>(st, ta)) != 0) {
+          PF::template resolve<REL>(st, sc[par], pr[par], ta);
           if (j != jfirst && __builtin_amdgcn_ballot_w64(st.alpha != 1.f) != 0) PF::repair(st.alpha);
         }
       }
