@@ -51,8 +51,9 @@ SIDE = {
     "prefill_alibi": "alibi_causal_prefill", "prefill_softcap": "softcap_causal_prefill",
     "prefill_window": "window_causal_prefill",
 }
-SWEEP_WORKLOAD = "mha_decode"
-SWEEP_SPLITS = (16, 32, 64)
+# decode split counts swept beside the library's choice: the per-head kernel
+# (MHA decode) and the grouped matrix-unit kernel (long GQA decode)
+SWEEPS = {"mha_decode": (16, 32, 64), "gqa_long_decode": (1, 2, 4, 8)}
 
 
 def kernel_source_hash(kind):
@@ -433,11 +434,14 @@ def main():
         results[name], errors[name] = run_norm(name, args.steps, args.warmup, errors=not args.no_errors)
         print(f"# {name}: {json.dumps(results[name])}", file=sys.stderr, flush=True)
     sweep = {}
-    for S in SWEEP_SPLITS:
-        r, _ = run_workload(SWEEP_WORKLOAD, args.steps, args.warmup, splits=S)
-        sweep[str(S)] = {"GB/s": r["GB/s"], "ms_per_step": r["ms_per_step"],
-                         "frac": round(r["GB/s"] / HBM_PEAK_GBS, 4),
-                         "frac_achievable": round(r["GB/s"] / peaks["hbm_read_GBs"], 4) if peaks else None}
+    for wname, splits in SWEEPS.items():
+        sweep[wname] = {"library_choice": results[wname]["num_splits"], "splits": {}}
+        for S in splits:
+            r, _ = run_workload(wname, args.steps, args.warmup, splits=S)
+            sweep[wname]["splits"][str(S)] = {
+                "GB/s": r["GB/s"], "ms_per_step": r["ms_per_step"],
+                "frac": round(r["GB/s"] / HBM_PEAK_GBS, 4),
+                "frac_achievable": round(r["GB/s"] / peaks["hbm_read_GBs"], 4) if peaks else None}
     print(f"# split sweep: {json.dumps(sweep)}", file=sys.stderr, flush=True)
 
     head = results[HEADLINE]
@@ -461,7 +465,7 @@ def main():
             entry = {"workload": name, "value": r["TFLOP/s"], "unit": "TFLOP/s", "ms_per_step": r["ms_per_step"],
                      "roofline": prefill_roofline(r, name, peaks, r["kernels"][0])}
         line[key] = entry
-    line["decode_split_sweep"] = {"workload": SWEEP_WORKLOAD, "splits": sweep}
+    line["decode_split_sweep"] = sweep
     line["norms"] = {name: {"workload": name, "value": results[name]["GB/s"], "unit": "GB/s",
                             "ms_per_step": results[name]["ms_per_step"],
                             "roofline": hbm_roofline(results[name], "norms", name, peaks,
