@@ -17,8 +17,10 @@ pair) and `roofline` its MFMA roofline, against the published dense fp16 peak
 and against the peak that an MFMA loop on random operands reaches on the same
 GPU in the same run (`achievable`, with the shader clock it held).  Beside it:
 the decode workloads as algorithmic GB/s (|Q|+|K|+|V|+|O|) against the HBM
-peak and the measured streaming-read rate, the other prefill workloads, a
-decode split-count sweep, the row reductions, error metrics of every workload
+peak and the measured streaming-read rate, the other prefill workloads, the
+row reductions, `split_sweep` (decode split counts of the per-head and the
+grouped kernel, chunks per row of the row reductions, each beside the
+library's choice), error metrics of every workload
 against the fp64 oracle (max, mean, RMS, p90, p99 of |GPU - oracle| on a
 stated sample), and `cpu_baseline`: the oracle timed on this host.
 """
@@ -54,6 +56,8 @@ SIDE = {
 # decode split counts swept beside the library's choice: the per-head kernel
 # (MHA decode) and the grouped matrix-unit kernel (long GQA decode)
 SWEEPS = {"mha_decode": (16, 32, 64), "gqa_long_decode": (1, 2, 4, 8)}
+# chunks per row swept beside the library's choice for the row reductions
+NORM_SWEEP = (1, 2, 4, 8, 16, 32)
 
 
 def kernel_source_hash(kind):
@@ -96,7 +100,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--only", default=None, help="run only this workload (for profiler passes)")
-    ap.add_argument("--splits", type=int, default=0, help="decode split count with --only (0: library)")
+    ap.add_argument("--splits", type=int, default=0, help="decode split count or norm chunks per row with --only (0: library)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -203,7 +207,7 @@ def run_workload(name, steps, warmup, *, splits=0, errors=False):
     return res, err
 
 
-def run_norm(name, steps, warmup, *, errors=False):
+def run_norm(name, steps, warmup, *, chunks=0, errors=False):
     import numpy as np
     import torch
     import paper_2510_08726_amd as pa
@@ -211,7 +215,11 @@ def run_norm(name, steps, warmup, *, errors=False):
 
     w = NORM_WORKLOADS[name]
     x = make_norm_input(w, device="cuda")
-    C = pa.norm_chunks(w.N, w.M, x.dtype)
+    C = chunks or pa.norm_chunks(w.N, w.M, x.dtype)
+    if w.op == "l2":
+        kernels = [f"norm_split_kernel<{w.dtype},0>", "l2_combine_kernel"]
+    else:
+        kernels = [f"norm_split_kernel<{w.dtype},1>", f"rms_apply_kernel<{w.dtype}>"]
     ws = torch.empty(pa.norm_workspace_bytes(w.N, C), dtype=torch.uint8, device="cuda")
     out = torch.empty(w.N, dtype=torch.float32, device="cuda")
     if w.op == "l2":
@@ -225,7 +233,8 @@ def run_norm(name, steps, warmup, *, errors=False):
     ms, wall_ms = time_steps(fn, steps, warmup)
     work = norm_bytes(w.op, w.N, w.M, x.element_size())
     gbs = work / (ms * 1e-3) / 1e9
-    res = {"op": w.op, "N": w.N, "M": w.M, "dtype": w.dtype, "chunks": C, "ms_per_step": round(ms, 5),
+    res = {"op": w.op, "N": w.N, "M": w.M, "dtype": w.dtype, "chunks": C, "kernels": kernels,
+           "ms_per_step": round(ms, 5),
            "host_wall_ms_per_step": round(wall_ms, 5), "bytes_per_step": work, "GB/s": round(gbs, 1),
            "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)}
     err = None
@@ -416,7 +425,7 @@ def main():
 
     if args.only:
         if args.only in NORM_WORKLOADS:
-            res, _ = run_norm(args.only, args.steps, args.warmup)
+            res, _ = run_norm(args.only, args.steps, args.warmup, chunks=args.splits)
         else:
             res, _ = run_workload(args.only, args.steps, args.warmup, splits=args.splits)
         if args.copy_mib:
@@ -442,6 +451,14 @@ def main():
                 "GB/s": r["GB/s"], "ms_per_step": r["ms_per_step"],
                 "frac": round(r["GB/s"] / HBM_PEAK_GBS, 4),
                 "frac_achievable": round(r["GB/s"] / peaks["hbm_read_GBs"], 4) if peaks else None}
+    for wname in NORM_WORKLOADS:
+        sweep[wname] = {"library_choice": results[wname]["chunks"], "chunks": {}}
+        for C in NORM_SWEEP:
+            r, _ = run_norm(wname, args.steps, args.warmup, chunks=C)
+            sweep[wname]["chunks"][str(C)] = {
+                "GB/s": r["GB/s"], "ms_per_step": r["ms_per_step"], "kernels": r["kernels"],
+                "frac": round(r["GB/s"] / HBM_PEAK_GBS, 4),
+                "frac_achievable": round(r["GB/s"] / peaks["hbm_read_GBs"], 4) if peaks else None}
     print(f"# split sweep: {json.dumps(sweep)}", file=sys.stderr, flush=True)
 
     head = results[HEADLINE]
@@ -465,7 +482,7 @@ def main():
             entry = {"workload": name, "value": r["TFLOP/s"], "unit": "TFLOP/s", "ms_per_step": r["ms_per_step"],
                      "roofline": prefill_roofline(r, name, peaks, r["kernels"][0])}
         line[key] = entry
-    line["decode_split_sweep"] = sweep
+    line["split_sweep"] = sweep
     line["norms"] = {name: {"workload": name, "value": results[name]["GB/s"], "unit": "GB/s",
                             "ms_per_step": results[name]["ms_per_step"],
                             "roofline": hbm_roofline(results[name], "norms", name, peaks,

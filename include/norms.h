@@ -45,7 +45,7 @@ typedef enum {
 } norm_dtype;
 
 /*
- * Chunks per row that the library uses when `chunks` is 0 (about 2048
+ * Chunks per row that the library uses when `chunks` is 0 (about 512
  * workgroups in all, chunks of at least 4096 elements).  Returns >= 1, or 0
  * for invalid sizes.
  */

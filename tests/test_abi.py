@@ -31,7 +31,7 @@ def declared_functions():
     for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
         src = open(os.path.join(ROOT, "include", h)).read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-        names.update(re.findall(r"\b((?:attn|peaks|norm)_[a-z0-9_]+|rmsnorm_rowmax)\s*\(", src))
+        names.update(re.findall(r"\b((?:attn|peaks|norm|rmsnorm)_[a-z0-9_]+)\s*\(", src))
     return sorted(names)
 
 
@@ -43,6 +43,18 @@ def test_every_declared_symbol_is_exported(lib):
             "norm_chunks", "norm_workspace_bytes"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
+
+
+def test_norm_chunk_heuristic(lib):
+    """Host logic of the row reductions' split: about 512 workgroups with
+    chunks of >= 4096 elements."""
+    F16, BF16, F32 = 0, 1, 2
+    assert lib.norm_chunks(256, 1 << 17, F32) == 2
+    assert lib.norm_chunks(256, 1 << 17, BF16) == 2
+    assert lib.norm_chunks(32, 1 << 10, F16) == 1           # chunks of >= 4096 elements
+    assert lib.norm_chunks(32, 1 << 17, F16) == 16          # 512 workgroups
+    assert lib.norm_chunks(1, 40000, BF16) == 10            # 512 / N, capped by M / 4096
+    assert lib.norm_chunks(0, 8, F16) == 0 and lib.norm_chunks(8, 8, 7) == 0
 
 
 def test_status_strings(lib):
