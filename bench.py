@@ -9,7 +9,9 @@ for a prefill workload (one kernel), attn_decode(_mod) for a decode workload
 (split kernel + combine kernel).  W untimed steps, then K steps timed with HIP
 events recorded on the stream the kernels are launched on (the current torch
 stream, which the binding passes to the library), bracketed by device
-synchronisation.  All inputs are resident in HBM before the timed region.
+synchronisation; `ms_per_step` is their mean.  K more steps, each between
+its own pair of events, give `launch_ms` (min and max per step).  All inputs
+are resident in HBM before the timed region.
 
 The headline line is the causal MHA prefill workload (B=4, H=32, L=2048,
 D=128, fp16): `value` is its algorithmic TFLOP/s (4*D per visible query/key
@@ -112,6 +114,9 @@ def parse():
 
 
 def time_steps(fn, steps, warmup):
+    """Mean ms per launch over `steps` back-to-back launches (HIP events on
+    the launch stream around all of them), the host wall time per launch, and
+    the min and max of `steps` more launches timed one by one."""
     import torch
     for _ in range(warmup):
         fn()
@@ -125,7 +130,14 @@ def time_steps(fn, steps, warmup):
     end.record()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / steps
-    return start.elapsed_time(end) / steps, wall
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in pairs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    each = [a.elapsed_time(b) for a, b in pairs]
+    return start.elapsed_time(end) / steps, wall, {"min_ms": round(min(each), 5), "max_ms": round(max(each), 5)}
 
 
 def _error_stats(got, ref):
@@ -187,11 +199,12 @@ def run_workload(name, steps, warmup, *, splits=0, errors=False):
                         softcap=w.softcap or None, window=w.window or None)
         work = prefill_flops(w.B, w.Hq, w.Lq, w.Lk, w.D, w.causal, w.window)
         kernels = pa.attn_fwd_kernels(w.D, q.dtype, w.causal, sl is not None, w.softcap, w.window)
-    ms, wall_ms = time_steps(fn, steps, warmup)
+    ms, wall_ms, each = time_steps(fn, steps, warmup)
     res = {
         "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk, "D": w.D, "dtype": w.dtype,
         "causal": w.causal, "alibi": w.alibi, "softcap": w.softcap, "window": w.window,
-        "kernels": kernels, "ms_per_step": round(ms, 5), "host_wall_ms_per_step": round(wall_ms, 5),
+        "kernels": kernels, "ms_per_step": round(ms, 5), "launch_ms": each,
+        "host_wall_ms_per_step": round(wall_ms, 5),
     }
     if w.decode:
         gbs = work / (ms * 1e-3) / 1e9
@@ -230,11 +243,11 @@ def run_norm(name, steps, warmup, *, chunks=0, errors=False):
 
         def fn():
             pa.rmsnorm_rowmax(x, y, out, eps=w.eps, chunks=C, workspace=ws)
-    ms, wall_ms = time_steps(fn, steps, warmup)
+    ms, wall_ms, each = time_steps(fn, steps, warmup)
     work = norm_bytes(w.op, w.N, w.M, x.element_size())
     gbs = work / (ms * 1e-3) / 1e9
     res = {"op": w.op, "N": w.N, "M": w.M, "dtype": w.dtype, "chunks": C, "kernels": kernels,
-           "ms_per_step": round(ms, 5),
+           "ms_per_step": round(ms, 5), "launch_ms": each,
            "host_wall_ms_per_step": round(wall_ms, 5), "bytes_per_step": work, "GB/s": round(gbs, 1),
            "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)}
     err = None
@@ -263,7 +276,7 @@ def achievable_peaks():
     buf.view(torch.float32).normal_()
     sink = pa.peaks_hbm_read(buf)
     torch.cuda.synchronize()
-    ms, _ = time_steps(lambda: pa.peaks_hbm_read(buf, sink), 10, 2)
+    ms, _, _ = time_steps(lambda: pa.peaks_hbm_read(buf, sink), 10, 2)
     out["hbm_read_GBs"] = round(buf.numel() / (ms * 1e-3) / 1e9, 1)
     out["hbm_read_frac_of_spec"] = round(out["hbm_read_GBs"] / HBM_PEAK_GBS, 4)
     del buf, sink
@@ -466,6 +479,7 @@ def main():
     line = {
         "metric": METRIC, "value": head["TFLOP/s"], "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "launch_ms": head["launch_ms"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
         "data": "synthetic",
         "config": {"workload": HEADLINE, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk,
