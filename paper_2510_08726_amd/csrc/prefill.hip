@@ -537,6 +537,13 @@ struct Prefill {
     static_for<pfd<IS_K>()>([&](auto ic) { read_frag<IS_K, decltype(ic)::value>(fr, tile, ad); });
   }
 
+  // First softmax step of MFMA slot s (plan P): none in the first kSoftLag
+  // slots, then the plan spread over the other NS - kSoftLag.
+  static constexpr int kSoftLag = 2;
+  static_assert(NS > kSoftLag, "slots left for the softmax steps");
+  template <typename P>
+  static constexpr int step_begin(int s) { return P::begin(s > kSoftLag ? s - kSoftLag : 0, NS - kSoftLag); }
+
   // Whole tiles after a wave's first one (SM 1 with P.V) take the relative
   // form in kernels with a bias or cap: every row of the wave has seen a key
   // by then (its own causal diagonal, or the whole first tile), so its
@@ -558,12 +565,15 @@ struct Prefill {
     constexpr bool PREP = LOG2 || MASKED;
     constexpr bool REL = rel(SM, PV);
     typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
-    // Every softmax step of the tile runs inside these NS slots, before the
+    // The softmax steps start kSoftLag slots into the iteration (the first
+    // slots issue only MFMAs, copies and operand reads; measured 1-2 % faster
+    // than starting at slot 0) and are spread over the remaining slots.
+    // Every step of the tile runs inside these NS slots, before the
     // lazy-rescale check reads the lane maximum and before the next
     // iteration's P.V reads the packed weights: a step left past the last
     // slot would leave P words unwritten (uninitialised registers on the
     // first tiles of an item) and the lane maximum incomplete.
-    static_assert(P::begin(0, NS) == 0 && P::begin(NS, NS) == P::NSTEP, "the steps cover the tile within the slots");
+    static_assert(step_begin<P>(0) == 0 && step_begin<P>(NS) == P::NSTEP, "the steps cover the tile within the slots");
     [&]<int... Ss>(std::integer_sequence<int, Ss...>) {
       (
           [&] {
@@ -597,7 +607,7 @@ struct Prefill {
                   M::template rowsum<kLAgpr>(make_uint2(p_prev.w[c16][2 * db], p_prev.w[c16][2 * db + 1]));
               }
             }
-            if constexpr (SM != 0) soft_range<P::begin(S, NS), P::begin(S + 1, NS), PREP, MASKED, REL>(st, s_cur, p_cur, ta);
+            if constexpr (SM != 0) soft_range<step_begin<P>(S), step_begin<P>(S + 1), PREP, MASKED, REL>(st, s_cur, p_cur, ta);
             __builtin_amdgcn_sched_barrier(0);
           }(),
           ...);
