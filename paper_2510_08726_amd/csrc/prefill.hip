@@ -162,7 +162,8 @@ constexpr int kAgprAlloc = (kOnesAgpr + 2 + 3) / 4 * 4;
 constexpr int kVgprBudget = 256 - kAgprAlloc;
 static_assert(kOnesAgpr + 2 == (kShardD == 64 ? 54 : 102), "the clobber list names every fixed AGPR");
 
-// 32x32x16 MFMAs.  qk0/qk: S^T accumulator in VGPRs (qk0 starts from zero), K
+// 32x32x16 MFMAs.  qk0/qk: S^T accumulator in VGPRs (qk0 starts from zero,
+// qk0c from the accumulator c), K
 // operand in VGPRs, Q operand from AGPRs a[QA .. QA + 3]; with PAD, two wait
 // states first, for an operand that the compiler reloads (VALU) just before.  pv: O^T accumulator
 // a[OA .. OA + 15], both operands in VGPRs.  rowsum: a 4x4x4 MFMA with the
@@ -186,6 +187,12 @@ template <> struct Mma<_Float16> {
     else
       asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
   }
+  template <int QA, bool PAD> static __device__ __forceinline__ void qk0c(f32x16& d, v8 a, const f32x16& c) {
+    if constexpr (PAD)
+      asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], %4" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3), "v"(c) : ATTN_AGPRS);
+    else
+      asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, a[%2:%3], %4" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3), "v"(c) : ATTN_AGPRS);
+  }
   template <int OA> static __device__ __forceinline__ void pv(v8 a, v8 b) {
     asm volatile("v_mfma_f32_32x32x16_f16 a[%2:%3], %0, %1, a[%2:%3]" : : "v"(a), "v"(b), "n"(OA), "n"(OA + 15) : ATTN_AGPRS);
   }
@@ -208,6 +215,12 @@ template <> struct Mma<__bf16> {
       asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
     else
       asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %0" : "+v"(d) : "v"(a), "n"(QA), "n"(QA + 3) : ATTN_AGPRS);
+  }
+  template <int QA, bool PAD> static __device__ __forceinline__ void qk0c(f32x16& d, v8 a, const f32x16& c) {
+    if constexpr (PAD)
+      asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %4" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3), "v"(c) : ATTN_AGPRS);
+    else
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, a[%2:%3], %4" : "=&v"(d) : "v"(a), "n"(QA), "n"(QA + 3), "v"(c) : ATTN_AGPRS);
   }
   template <int OA> static __device__ __forceinline__ void pv(v8 a, v8 b) {
     asm volatile("v_mfma_f32_32x32x16_bf16 a[%2:%3], %0, %1, a[%2:%3]" : : "v"(a), "v"(b), "n"(OA), "n"(OA + 15) : ATTN_AGPRS);
@@ -253,7 +266,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 //   exp    8 steps: 2 exponentials and their packing
 //   max    4 steps: 4 scores folded into this lane's partial max
 // (the exp-sum is accumulated by rowsum MFMAs beside P.V).
-template <bool PREP, bool MASKED, bool ALIBI, bool CAP>
+template <bool PREP, bool MASKED, bool ALIBI, bool CAP, bool ACCB = false>
 struct SoftPlan {
   // Steps [0, MAX0) prepare the scores, four registers a step; then come 8
   // exponential steps (two registers each) and 4 steps of the lane's running
@@ -264,7 +277,7 @@ struct SoftPlan {
   static constexpr int exp_index(int k) { return 2 * ((k - MAX0) / 3) + (k - MAX0) % 3; }
   static constexpr int max_index(int k) { return (k - MAX0) / 3; }
   static constexpr int weight(int k) {
-    if (k < MAX0) return (ALIBI ? 8 : 0) + (MASKED ? 8 : 0) + (CAP ? 52 : 0);
+    if (k < MAX0) return (ALIBI ? (ACCB ? 4 : 8) : 0) + (MASKED ? 8 : 0) + (CAP ? 52 : 0);
     return is_exp(k) ? 26 : 10;
   }
   // First step of slot s when the steps are spread over ns slots.
@@ -285,6 +298,11 @@ struct Prefill {
   // Scores are prepared in log2 units (the scale folded in) whenever a bias
   // or the cap has to act on the scaled value.
   static constexpr bool LOG2 = ALIBI || CAP;
+  // ALiBi at D = 64: the key-dependent part of the bias starts the S^T
+  // accumulator (kb, per work item), so preparing a score takes one FMA with
+  // the tile's per-row base instead of computing the bias first.  (At
+  // D = 128 the 16 registers of kb do not fit.)
+  static constexpr bool ACCB = ALIBI && D == 64;
   typedef Elem<T> E;
   typedef Mma<T> M;
   typedef typename E::vec8 vec8;
@@ -303,7 +321,7 @@ struct Prefill {
   // with ALiBi or SoftCap (more live state), one V fragment; deeper rings
   // push the per-item code into scratch.  At D = 64 the smaller AGPR share
   // leaves room for three of each.
-  static constexpr int PFD_K = D == 64 ? 3 : 1;
+  static constexpr int PFD_K = D == 64 && !ACCB ? 3 : 1;
   static constexpr int PFD_V = (LOG2 || WIN) ? 1 : 3;
   template <bool IS_K> static constexpr int pfd() { return IS_K ? PFD_K : PFD_V; }
   static_assert(NG % (PFD_K + 1) == 0 && NG % (PFD_V + 1) == 0, "fragment ring positions must repeat every iteration");
@@ -334,6 +352,7 @@ struct Prefill {
     float sl2;    // ALiBi slope * log2(e)
     float abase;  // ALiBi bias of key j0 + 4 hh relative to the wave's first row
     float mb;     // (ALiBi bias base, or SoftCap cl) minus the row's reference max
+    f32x16 kb;    // ACCB: slope * log2(e) * kconst(r) / c, the start of each S^T accumulator
     int lim;      // last visible key offset (key - j0 - 4 hh) of this lane's row
     int llo;      // first visible key offset of this lane's row (sliding window)
     float t;      // this lane's maximum score of the tile
@@ -422,7 +441,7 @@ struct Prefill {
   // and the lazy check work relative to m.
   template <int K, bool PREP, bool MASKED, bool REL>
   static __device__ __forceinline__ void soft_step(State& st, Scores& sc, Probs& pr, TileArgs& ta) {
-    typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
+    typedef SoftPlan<PREP, MASKED, ALIBI, CAP, ACCB> P;
     const float ce = LOG2 ? 1.f : ta.c;
     static_assert(!REL || (LOG2 && !MASKED), "the relative form is for whole tiles with a bias or cap");
     if constexpr (K < P::MAX0) {
@@ -430,7 +449,11 @@ struct Prefill {
       // Registers r0 .. r0 + 3 hold keys kconst(r0) + 0..3: their biases are
       // the bias of the first plus 0..3 slopes.
       [[maybe_unused]] float b[4] = {0.f, 0.f, 0.f, 0.f};
-      if constexpr (ALIBI) {
+      if constexpr (ALIBI && ACCB) {
+        // sc already holds s + kb = s + slope log2(e) kconst(r) / c.
+        const float base = REL ? ta.mb : ta.abase;
+        b[0] = b[1] = b[2] = b[3] = base;
+      } else if constexpr (ALIBI) {
         const float base = REL ? ta.mb : ta.abase;
         b[0] = r0 == 0 ? base : __builtin_fmaf(ta.sl2, (float)kconst(r0), base);
         b[1] = b[0] + ta.sl2;
@@ -487,7 +510,7 @@ struct Prefill {
   // reference and factor 1.
   template <bool REL>
   static __device__ __forceinline__ void resolve(State& st, Scores& sc, Probs& pr, TileArgs& ta) {
-    typedef SoftPlan<false, false, ALIBI, CAP> P;
+    typedef SoftPlan<false, false, ALIBI, CAP, ACCB> P;
     const float ce = LOG2 ? 1.f : ta.c;
     const float tm = max_halves(ta.t);
     const float d = REL ? tm : __builtin_fmaf(tm, ce, -st.mc);
@@ -564,7 +587,7 @@ struct Prefill {
     constexpr bool MASKED = SM == 2;
     constexpr bool PREP = LOG2 || MASKED;
     constexpr bool REL = rel(SM, PV);
-    typedef SoftPlan<PREP, MASKED, ALIBI, CAP> P;
+    typedef SoftPlan<PREP, MASKED, ALIBI, CAP, ACCB> P;
     // The softmax steps start kSoftLag slots into the iteration (the first
     // slots issue only MFMAs, copies and operand reads; measured 1-2 % faster
     // than starting at slot 0) and are spread over the remaining slots.
@@ -590,7 +613,8 @@ struct Prefill {
                 // Without the causal mask the kernel has the register
                 // pressure at which the compiler parks K operands in spare
                 // AGPRs and reloads them right before their MFMA.
-                if constexpr (i == 0) M::template qk0<qagpr(i), !CAUSAL>(s_next, fk[i % (PFD_K + 1)]);
+                if constexpr (i == 0 && ACCB) M::template qk0c<qagpr(i), !CAUSAL>(s_next, fk[i % (PFD_K + 1)], ta.kb);
+                else if constexpr (i == 0) M::template qk0<qagpr(i), !CAUSAL>(s_next, fk[i % (PFD_K + 1)]);
                 else M::template qk<qagpr(i), !CAUSAL>(s_next, fk[i % (PFD_K + 1)]);
               }
             } else {
@@ -870,6 +894,16 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
     TileArgs ta;
     ta.c = p.c;
     ta.sl2 = ALIBI ? p.slopes[cur.hq] * kLog2e : 0.f;
+    if constexpr (PF::ACCB) {
+      // c (s + kb) + base = c s + slope log2(e) kconst(r) + base.  A zero
+      // scale takes a tiny c instead, whose product with s vanishes.
+      if (ta.c == 0.f) ta.c = 1e-30f;
+      const float ik = 1.f / ta.c;
+      static_for<16>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        ta.kb[r] = ta.sl2 * (float)PF::kconst(r) * ik;
+      });
+    }
     ta.k2 = p.cap_k2;
     ta.cl = p.cap_cl;
     ta.t = kNegInf;
