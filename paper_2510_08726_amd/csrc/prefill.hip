@@ -348,7 +348,7 @@ struct Prefill {
   };
   struct TileArgs {
     float c;      // scale * log2(e) (with ALiBi or SoftCap) or max(|scale| * log2(e), tiny)
-    float k2, cl; // SoftCap: 2 / cap and cap * log2(e)
+    float k2, cl; // SoftCap: 2 c / cap (c folded in) and cap * log2(e)
     float sl2;    // ALiBi slope * log2(e)
     float abase;  // ALiBi bias of key j0 + 4 hh relative to the wave's first row
     float mb;     // (ALiBi bias base, or SoftCap cl) minus the row's reference max
@@ -463,7 +463,7 @@ struct Prefill {
 #pragma unroll
       for (int r = r0; r < r0 + 4; ++r) {
         if constexpr (CAP) {
-          const float x = soft_cap(sc[r] * ta.c, ta.k2, ta.cl, REL && !ALIBI ? ta.mb : ta.cl);
+          const float x = soft_cap(sc[r], ta.k2, ta.cl, REL && !ALIBI ? ta.mb : ta.cl);
           sc[r] = ALIBI ? x + b[r - r0] : x;
         } else if constexpr (ALIBI) {
           sc[r] = __builtin_fmaf(sc[r], ta.c, b[r - r0]);
@@ -904,7 +904,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
         ta.kb[r] = ta.sl2 * (float)PF::kconst(r) * ik;
       });
     }
-    ta.k2 = p.cap_k2;
+    ta.k2 = p.cap_k2 * ta.c;   // the scale folded into the cap's exponent
     ta.cl = p.cap_cl;
     ta.t = kNegInf;
     // Per-tile softmax parameters of tile(j).
