@@ -484,9 +484,10 @@ struct Prefill {
       pr.w[r / 8][(r % 8) / 2] = w;
     } else {
       constexpr int q = P::max_index(K);
-      const float m4 = fmaxf(fmaxf(sc[4 * q], sc[4 * q + 1]), fmaxf(sc[4 * q + 2], sc[4 * q + 3]));
-      if constexpr (q == 0) ta.t = m4;
-      else ta.t = fmaxf(ta.t, m4);
+      // A running chain: two v_max3 a step (the tree of four and a fold
+      // took one more).
+      if constexpr (q == 0) ta.t = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), sc[2]), sc[3]);
+      else ta.t = fmaxf(fmaxf(fmaxf(fmaxf(ta.t, sc[4 * q]), sc[4 * q + 1]), sc[4 * q + 2]), sc[4 * q + 3]);
       pin(ta.t);
     }
   }
