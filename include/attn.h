@@ -80,6 +80,8 @@ typedef enum {
  *
  *   Q [B, Hq, Lq, D], K and V [B, Hkv, Lk, D], O [B, Hq, Lq, D]   (device)
  *   B, Hq, Hkv, Lq, Lk >= 1; Hq % Hkv == 0; D in {64, 128}
+ *   Lk * D * 2 < 2^31 (one head's K or V in bytes; Lk < 8388608 at D = 128),
+ *   and B * Hq * Lq * D, B * Hkv * Lk * D < 2^40
  *   causal  0 or 1 (non-zero means 1)
  *   scale   finite float
  *   alibi_slopes  device float[Hq] or NULL

@@ -98,6 +98,8 @@ int attn_fwd_mod(const void* Q, const void* K, const void* V, void* O,
   if (softcap > 0.f && (!causal || alibi_slopes)) return ATTN_ERR_UNSUPPORTED;
   if (window > 0 && !causal) return ATTN_ERR_UNSUPPORTED;
   if (!sizes_fit(B, Hq, Hkv, Lq, Lk, D)) return ATTN_ERR_SHAPE;
+  // The prefill kernel addresses one head's K and V with 32-bit byte offsets.
+  if ((int64_t)Lk * D * 2 >= (int64_t(1) << 31)) return ATTN_ERR_SHAPE;
   const int bm = attn::prefill_block_rows();
   const int64_t nqb = ((int64_t)Lq + bm - 1) / bm;
   if (nqb * B * Hq > kMaxGrid) return ATTN_ERR_SHAPE;

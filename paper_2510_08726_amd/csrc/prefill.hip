@@ -378,6 +378,29 @@ struct Prefill {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  : : "s"(slot + (uint32_t)(blk * 1024)), "v"(dof), "s"(rsrc) : "memory", "m0");
   }
+  // The buffer resource of one head's K or V for a work item: base = the
+  // head's first row, range = the item's staged rows (`rows`, in bytes).
+  static __device__ __forceinline__ u32x4 head_rsrc(const T* base, int rows) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
+                 (uint32_t)__builtin_amdgcn_readfirstlane(rows * D * (int)sizeof(T)), 0x00020000u};
+  }
+  // The same copy as copy_block through a head's resource: the tile offset
+  // goes into the lane offset, which the buffer range check covers, so rows
+  // past the range, tiles past it and negative tiles (whose offsets wrap to
+  // above 2^31) read as zero.  Per copy, one VALU add and the m0 write; the
+  // host keeps Lk * D * sizeof(T) below 2^31.
+  static __device__ __forceinline__ void copy_tile(const u32x4& rs, uint32_t slot, int t, int blk, int dof) {
+    // The tile's byte offset passes through an opaque scalar copy, so that
+    // the add happens here rather than being hoisted out of the unrolled
+    // loop into a register per copy.
+    int tb = __builtin_amdgcn_readfirstlane(t * (TE * (int)sizeof(T)));
+    asm volatile("" : "+s"(tb));
+    const int off = dof + tb;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 : : "s"(slot + (uint32_t)(blk * 1024)), "v"(off), "s"(rs) : "memory", "m0");
+  }
   // Copy u of a wave moves a block of the K tile (else of the V tile).
   static __device__ __forceinline__ bool copies_k(int u, int wave) {
     return NB >= kWaves ? u * kWaves < NB : wave < NB;
@@ -801,17 +824,17 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
   // 0 .. kRing-4, each wave its blocks.  Issued once the previous item's last barrier has
   // passed (every ring slot is free then), before that item's output.
   auto stage_kv = [&](const Item& it) __attribute__((always_inline)) {
-    const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)it.kvh * Lk * D;
-    const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)it.kvh * Lk * D;
+    const u32x4 rk = PF::head_rsrc(reinterpret_cast<const T*>(p.k) + (size_t)it.kvh * Lk * D, it.rows);
+    const u32x4 rv = PF::head_rsrc(reinterpret_cast<const T*>(p.v) + (size_t)it.kvh * Lk * D, it.rows);
 #pragma unroll
     for (int u = 0; u < CPW; ++u) {
       const int b = (u * kWaves + wave) % NB;
       if (PF::copies_k(u, wave)) {
 #pragma unroll
-        for (int t = 0; t < kRing - 1; ++t) PF::copy_block(kp, it.rows, kslot(t), tile_of(it, t), b, dof[u]);
+        for (int t = 0; t < kRing - 1; ++t) PF::copy_tile(rk, kslot(t), tile_of(it, t), b, dof[u]);
       } else {
 #pragma unroll
-        for (int t = 0; t < kRing - 3; ++t) PF::copy_block(vp, it.rows, vslot(t), tile_of(it, t), b, dof[u]);
+        for (int t = 0; t < kRing - 3; ++t) PF::copy_tile(rv, vslot(t), tile_of(it, t), b, dof[u]);
       }
     }
   };
@@ -843,8 +866,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
     const int nt = cur.t1 - cur.t0;   // iterations with a tile
     const int iw = cur.iw;
     const int row = iw + n;           // this lane's query row
-    const T* kp = reinterpret_cast<const T*>(p.k) + (size_t)cur.kvh * Lk * D;
-    const T* vp = reinterpret_cast<const T*>(p.v) + (size_t)cur.kvh * Lk * D;
+    const u32x4 rk = PF::head_rsrc(reinterpret_cast<const T*>(p.k) + (size_t)cur.kvh * Lk * D, cur.rows);
+    const u32x4 rv = PF::head_rsrc(reinterpret_cast<const T*>(p.v) + (size_t)cur.kvh * Lk * D, cur.rows);
     auto tile = [&](int j) __attribute__((always_inline)) { return tile_of(cur, j); };
     // Copy u of this wave in iteration j: its block of K tile(j + kRing) into
     // K slot j mod kRing (whose tile j was last read in iteration j - 1), or
@@ -854,8 +877,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
       constexpr int k = decltype(slotc)::value % kRing;
       constexpr int u = decltype(uc)::value;
       const int b = (u * kWaves + wave) % NB;
-      if (PF::copies_k(u, wave)) PF::copy_block(kp, cur.rows, kslot(k), tile(j + kRing), b, dof[u]);
-      else PF::copy_block(vp, cur.rows, vslot((k + kRing - 2) % kRing), tile(j + kRing - 2), b, dof[u]);
+      if (PF::copies_k(u, wave)) PF::copy_tile(rk, kslot(k), tile(j + kRing), b, dof[u]);
+      else PF::copy_tile(rv, vslot((k + kRing - 2) % kRing), tile(j + kRing - 2), b, dof[u]);
     };
     // Iterations j in [j0, j1), j0 >= -1, of one variant; the loop body is
     // unrolled by kUnroll so that slots and parities are compile-time choices.

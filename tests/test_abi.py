@@ -91,6 +91,8 @@ def fwd(lib, q=FAKE, k=FAKE, v=FAKE, o=FAKE, B=1, Hq=2, Hkv=2, Lq=8, Lk=8, D=64,
     (dict(causal=1, window=4, q=NULL), pa.ATTN_ERR_NULL),
     (dict(dtype=2), pa.ATTN_ERR_UNSUPPORTED),
     (dict(B=1 << 20, Hq=1 << 10, Hkv=1 << 10, Lq=1 << 20, Lk=1 << 20), pa.ATTN_ERR_SHAPE),
+    # one head's K or V must stay below 2^31 bytes (32-bit offsets in the prefill copies)
+    (dict(Lk=1 << 23, D=128), pa.ATTN_ERR_SHAPE), (dict(Lk=1 << 24, D=64), pa.ATTN_ERR_SHAPE),
 ])
 def test_fwd_rejects_bad_arguments(lib, kw, code):
     assert fwd(lib, **kw) == code
