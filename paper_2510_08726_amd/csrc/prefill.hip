@@ -358,15 +358,15 @@ struct Prefill {
     float t;      // this lane's maximum score of the tile
   };
 
-  // HBM -> LDS copy of 1 KB block `blk` of key/value tile t (rows t BN ..
-  // t BN + BN - 1) of one head (base) into the LDS slot at byte address
-  // `slot`; dof is the lane's byte offset within the tile.  The buffer range
-  // ends at row `rows` (the workgroup's last staged row) or at the tile's
-  // end, whichever comes first, so rows past it read as zero, and a tile
-  // past it (or a negative one) has an empty range and writes zeros.  The tile offset lives in the (scalar) buffer base, so the lane
-  // offset is the same register for every tile.  Issued as inline assembly:
-  // the compiler then adds no waits of its own for the LDS writes; the kernel
-  // waits for them explicitly before its barriers.
+  // HBM -> LDS copy of 1 KB block `blk` of tile t (rows t BN .. t BN + BN -
+  // 1) of one head (base) into the LDS slot at byte address `slot`; dof is
+  // the lane's byte offset within the tile.  The buffer range ends at row
+  // `rows` or at the tile's end, whichever comes first, so rows past it read
+  // as zero, and a tile past it (or a negative one) has an empty range and
+  // writes zeros.  The tile offset lives in the (scalar) buffer base.  Used
+  // for the Q rows of a work item; K and V go through copy_tile.  Issued as
+  // inline assembly: the compiler then adds no waits of its own for the LDS
+  // writes; the kernel waits for them explicitly before its barriers.
   static __device__ __forceinline__ void copy_block(const T* base, int rows, uint32_t slot, int t, int blk, int dof) {
     const int left = t >= 0 ? max(rows - t * BN, 0) : 0;
     const uint64_t a = reinterpret_cast<uint64_t>(base + (left > 0 ? (size_t)t * TE : 0));
