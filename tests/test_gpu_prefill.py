@@ -57,7 +57,8 @@ def test_prefill_matches_oracle(case):
         assert torch.all(o[:, :, :Lq - Lk] == 0)
 
 
-@pytest.mark.parametrize("scale,alibi", [(0.0, False), (0.0, True), (-0.2, False), (-0.2, True), (3.0, False)])
+@pytest.mark.parametrize("scale,alibi", [(0.0, False), (0.0, True), (-0.2, False), (-0.2, True), (3.0, False),
+                                         (3.0, True)])
 def test_prefill_special_scales(scale, alibi):
     """scale 0 (uniform / geometric weights), negative scale, large scores."""
     B, H, L, D = 1, 4, 200, 64
