@@ -24,7 +24,7 @@
 //   l = a l + rowsum P(j-1)            row sums by 4x4x4 MFMAs
 //
 // with the two kinds of MFMA alternating slot by slot and the softmax steps
-// of tile j spread over the same slots, so that the VALU work of a wave
+// of tile j spread over the same slots from the third on, so that the VALU work of a wave
 // issues while its own MFMAs run (within one wave the matrix unit and the
 // VALU overlap almost completely; across the two waves of a SIMD the same
 // mix overlaps far less).  The factor a = exp2(m - m') is applied only when
@@ -39,7 +39,8 @@
 //
 // The K and V tiles of the workgroup pass through LDS rings of kRing slots,
 // filled by buffer loads with the LDS bit (HBM -> LDS without VGPRs) that all
-// waves issue, kRing - 1 tiles ahead of their use; one barrier per iteration
+// waves issue in the P.V slots, kRing - 1 tiles ahead of their use, through
+// one buffer resource per head and work item; one barrier per iteration
 // publishes them.  Between work items each wave borrows one ring slot that
 // the next item's first copies leave free: its O rows go out and its next
 // Q rows come in through it, as whole 1 KB blocks.
@@ -56,7 +57,8 @@
 // relative to another reference point; the final division by l cancels it.
 //
 // Scores are in log2 units: t = s * scale * log2(e) (+ ALiBi bias * log2(e)),
-// so each exponential is one v_exp_f32.
+// so each exponential is one v_exp_f32.  With ALiBi at D = 64 the key part of
+// the bias starts the S^T accumulator, so that preparing a score is one FMA.
 
 #include <algorithm>
 #include <atomic>
