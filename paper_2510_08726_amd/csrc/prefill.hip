@@ -203,6 +203,14 @@ template <> struct Mma<_Float16> {
     asm volatile("v_mfma_f32_4x4x4_16b_f16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
                  : : "v"(b), "n"(LA), "n"(LA + 3), "n"(kOnesAgpr), "n"(kOnesAgpr + 1) : ATTN_AGPRS);
   }
+  // Clear 16 (zero16) or 4 (zero4) AGPRs: an MFMA with zero operands and C = 0
+  // (two wait states first: the zero operand is written just before).
+  template <int A> static __device__ __forceinline__ void zero16(v8 z) {
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_f16 a[%1:%2], %0, %0, 0" : : "v"(z), "n"(A), "n"(A + 15) : ATTN_AGPRS);
+  }
+  template <int A> static __device__ __forceinline__ void zero4(uint2 z) {
+    asm volatile("s_nop 1\n\tv_mfma_f32_4x4x4_16b_f16 a[%1:%2], %0, %0, 0" : : "v"(z), "n"(A), "n"(A + 3) : ATTN_AGPRS);
+  }
 };
 template <> struct Mma<__bf16> {
   typedef bf16x8 v8;
@@ -231,6 +239,14 @@ template <> struct Mma<__bf16> {
   template <int LA> static __device__ __forceinline__ void rowsum(uint2 b) {
     asm volatile("v_mfma_f32_4x4x4_16b_bf16 a[%1:%2], a[%3:%4], %0, a[%1:%2]"
                  : : "v"(b), "n"(LA), "n"(LA + 3), "n"(kOnesAgpr), "n"(kOnesAgpr + 1) : ATTN_AGPRS);
+  }
+  // Clear 16 (zero16) or 4 (zero4) AGPRs: an MFMA with zero operands and C = 0
+  // (two wait states first: the zero operand is written just before).
+  template <int A> static __device__ __forceinline__ void zero16(v8 z) {
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 a[%1:%2], %0, %0, 0" : : "v"(z), "n"(A), "n"(A + 15) : ATTN_AGPRS);
+  }
+  template <int A> static __device__ __forceinline__ void zero4(uint2 z) {
+    asm volatile("s_nop 1\n\tv_mfma_f32_4x4x4_16b_bf16 a[%1:%2], %0, %0, 0" : : "v"(z), "n"(A), "n"(A + 3) : ATTN_AGPRS);
   }
 };
 
@@ -904,16 +920,34 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) __attribute__((amdgpu_num_vgpr(
     // from being hoisted out of the item loop.)
     int zero = 0;
     pin(zero);
-    static_for<KX>([&](auto ic) {
-      constexpr int kx = decltype(ic)::value;
-      const u32x4 w = __builtin_bit_cast(u32x4, PF::kfrag(xl + zero, ad, kx));
-      agpr_write<PF::qagpr(kx) + 0>(w[0] ^ p.qsign);
-      agpr_write<PF::qagpr(kx) + 1>(w[1] ^ p.qsign);
-      agpr_write<PF::qagpr(kx) + 2>(w[2] ^ p.qsign);
-      agpr_write<PF::qagpr(kx) + 3>(w[3] ^ p.qsign);
-    });
-    static_for<DB * 16>([&](auto ic) { agpr_zero<kOAgpr + decltype(ic)::value>(); });
-    static_for<4>([&](auto ic) { agpr_zero<kLAgpr + decltype(ic)::value>(); });
+    if (p.qsign == 0) {
+      // Straight from LDS into the AGPRs (the barrier below waits for them).
+      static_for<KX>([&](auto ic) {
+        constexpr int kx = decltype(ic)::value;
+        const uint32_t a = xslot + (uint32_t)(zero + ad.k[kx]);
+        asm volatile("ds_read_b128 a[%1:%2], %0" : : "v"(a), "n"(PF::qagpr(kx)), "n"(PF::qagpr(kx) + 3)
+                     : "memory", ATTN_AGPRS);
+      });
+    } else {
+      static_for<KX>([&](auto ic) {
+        constexpr int kx = decltype(ic)::value;
+        const u32x4 w = __builtin_bit_cast(u32x4, PF::kfrag(xl + zero, ad, kx));
+        agpr_write<PF::qagpr(kx) + 0>(w[0] ^ p.qsign);
+        agpr_write<PF::qagpr(kx) + 1>(w[1] ^ p.qsign);
+        agpr_write<PF::qagpr(kx) + 2>(w[2] ^ p.qsign);
+        agpr_write<PF::qagpr(kx) + 3>(w[3] ^ p.qsign);
+      });
+    }
+    // O^T and l start at zero: one MFMA with zero operands and C = 0 clears
+    // 16 AGPRs (68 AGPR writes otherwise).
+    {
+      typename PF::M::v8 z8 = {};
+      pin(z8);
+      static_for<DB>([&](auto dc) { PF::M::template zero16<PF::oagpr(decltype(dc)::value)>(z8); });
+      uint2 z2 = make_uint2(0u, 0u);
+      pin(z2);
+      PF::M::template zero4<kLAgpr>(z2);
+    }
     State st;
     st.mc = kMcInit;
     st.alpha = 1.f;
