@@ -13,6 +13,13 @@ synchronisation; `ms_per_step` is their mean.  K more steps, each between
 its own pair of events, give `launch_ms` (min and max per step).  All inputs
 are resident in HBM before the timed region.
 
+The HBM-bound workloads (decode, row reductions) take their inputs in turn
+from copies that span at least 2 GiB, so that no step finds its input in the
+256 MB memory-side cache (Infinity Cache) that the previous steps filled:
+their `GB/s` is the rate from HBM.  `GB/s_same_input` is the rate with one
+input read by every step, as a caller that re-reads a cache-resident tensor
+would see it.
+
 The headline line is the causal MHA prefill workload (B=4, H=32, L=2048,
 D=128, fp16): `value` is its algorithmic TFLOP/s (4*D per visible query/key
 pair) and `roofline` its MFMA roofline, against the published dense fp16 peak
@@ -60,6 +67,13 @@ SIDE = {
 SWEEPS = {"mha_decode": (16, 32, 64), "gqa_long_decode": (1, 2, 4, 8)}
 # chunks per row swept beside the library's choice for the row reductions
 NORM_SWEEP = (1, 2, 4, 8, 16, 32)
+# input bytes that the HBM-bound workloads rotate through, 8x the memory-side cache
+COLD_BYTES = 2 << 30
+
+
+def input_copies(nbytes):
+    """Copies of an input of `nbytes` that span COLD_BYTES (at least 2)."""
+    return max(2, -(-COLD_BYTES // nbytes))
 
 
 def kernel_source_hash(kind):
@@ -116,24 +130,27 @@ def parse():
 def time_steps(fn, steps, warmup):
     """Mean ms per launch over `steps` back-to-back launches (HIP events on
     the launch stream around all of them), the host wall time per launch, and
-    the min and max of `steps` more launches timed one by one."""
+    the min and max of `steps` more launches timed one by one.  `fn` is a
+    callable or a list of callables that successive steps take in turn."""
     import torch
-    for _ in range(warmup):
-        fn()
+    fns = list(fn) if isinstance(fn, (list, tuple)) else [fn]
+    n = len(fns)
+    for i in range(warmup):
+        fns[i % n]()
     torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record()
-    for _ in range(steps):
-        fn()
+    for i in range(steps):
+        fns[i % n]()
     end.record()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / steps
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for a, b in pairs:
+    for i, (a, b) in enumerate(pairs):
         a.record()
-        fn()
+        fns[i % n]()
         b.record()
     torch.cuda.synchronize()
     each = [a.elapsed_time(b) for a, b in pairs]
@@ -185,11 +202,13 @@ def run_workload(name, steps, warmup, *, splits=0, errors=False):
         S = splits or w.num_splits or pa.attn_decode_num_splits(w.B, w.Hq, w.Hkv, w.Lk, w.D)
         ws = torch.empty(pa.attn_decode_workspace_bytes(w.B, w.Hq, w.D, S), dtype=torch.uint8,
                          device="cuda")
-
-        def fn():
-            pa.attn_decode(q, k, v, o, scale=w.sm_scale, alibi_slopes=sl, softcap=w.softcap or None,
-                           num_splits=S, workspace=ws)
         work = decode_bytes(w.B, w.Hq, w.Hkv, w.Lk, w.D)
+        sets = [(q, k, v)] + [(q.clone(), k.clone(), v.clone()) for _ in range(input_copies(work) - 1)]
+
+        def step(qs, ks, vs):
+            return lambda: pa.attn_decode(qs, ks, vs, o, scale=w.sm_scale, alibi_slopes=sl,
+                                          softcap=w.softcap or None, num_splits=S, workspace=ws)
+        fn = [step(*t) for t in sets]
         kernels = pa.attn_decode_kernels(w.Hq, w.Hkv, w.D, q.dtype, sl is not None, w.softcap)
     else:
         S = None
@@ -200,6 +219,7 @@ def run_workload(name, steps, warmup, *, splits=0, errors=False):
         work = prefill_flops(w.B, w.Hq, w.Lq, w.Lk, w.D, w.causal, w.window)
         kernels = pa.attn_fwd_kernels(w.D, q.dtype, w.causal, sl is not None, w.softcap, w.window)
     ms, wall_ms, each = time_steps(fn, steps, warmup)
+    ms_same = time_steps(fn[0], steps, warmup)[0] if w.decode else None
     res = {
         "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk, "D": w.D, "dtype": w.dtype,
         "causal": w.causal, "alibi": w.alibi, "softcap": w.softcap, "window": w.window,
@@ -209,12 +229,15 @@ def run_workload(name, steps, warmup, *, splits=0, errors=False):
     if w.decode:
         gbs = work / (ms * 1e-3) / 1e9
         res.update({"num_splits": S, "bytes_per_step": work, "GB/s": round(gbs, 1),
-                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)})
+                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2), "input_copies": len(sets),
+                    "GB/s_same_input": round(work / (ms_same * 1e-3) / 1e9, 1)})
     else:
         tf = work / (ms * 1e-3) / 1e12
         res.update({"flops_per_step": work, "TFLOP/s": round(tf, 2),
                     "pct_mfma_peak": round(100 * tf / MFMA_PEAK_TFLOPS, 2)})
     err = attention_errors(w, q, k, v, sl, o) if errors else None
+    if w.decode:
+        del sets, fn
     del q, k, v, o
     torch.cuda.empty_cache()
     return res, err
@@ -235,21 +258,26 @@ def run_norm(name, steps, warmup, *, chunks=0, errors=False):
         kernels = [f"norm_split_kernel<{w.dtype},1>", f"rms_apply_kernel<{w.dtype}>"]
     ws = torch.empty(pa.norm_workspace_bytes(w.N, C), dtype=torch.uint8, device="cuda")
     out = torch.empty(w.N, dtype=torch.float32, device="cuda")
+    xs = [x] + [x.clone() for _ in range(input_copies(x.numel() * x.element_size()) - 1)]
     if w.op == "l2":
-        def fn():
-            pa.norm_l2(x, out, chunks=C, workspace=ws)
+        def step(xi):
+            return lambda: pa.norm_l2(xi, out, chunks=C, workspace=ws)
     else:
         y = torch.empty_like(x)
 
-        def fn():
-            pa.rmsnorm_rowmax(x, y, out, eps=w.eps, chunks=C, workspace=ws)
+        def step(xi):
+            return lambda: pa.rmsnorm_rowmax(xi, y, out, eps=w.eps, chunks=C, workspace=ws)
+    fn = [step(xi) for xi in xs]
     ms, wall_ms, each = time_steps(fn, steps, warmup)
+    ms_same = time_steps(fn[0], steps, warmup)[0]
     work = norm_bytes(w.op, w.N, w.M, x.element_size())
     gbs = work / (ms * 1e-3) / 1e9
     res = {"op": w.op, "N": w.N, "M": w.M, "dtype": w.dtype, "chunks": C, "kernels": kernels,
            "ms_per_step": round(ms, 5), "launch_ms": each,
            "host_wall_ms_per_step": round(wall_ms, 5), "bytes_per_step": work, "GB/s": round(gbs, 1),
-           "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)}
+           "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2), "input_copies": len(xs),
+           "GB/s_same_input": round(work / (ms_same * 1e-3) / 1e9, 1)}
+    del xs, fn
     err = None
     if errors:
         from oracle import norms

@@ -6,6 +6,11 @@
 // privatised local reduction), the 256 lanes' states are combined with the
 // same repair, and the chunk partials of a row are combined by the second
 // kernel.
+//
+// Cache policy: X is read once by the L2 norm and last by RMSNorm's second
+// kernel, so those loads (and the stores of y) are nontemporal; RMSNorm's
+// first pass reads X with ordinary loads so that the second pass finds what
+// the caches (L2 and the memory-side cache) still hold of it.
 
 #include <type_traits>
 
@@ -17,7 +22,14 @@ namespace attn {
 namespace {
 
 constexpr int kNormThreads = 256;
-constexpr int kNormUnroll = 4;   // 16-byte loads in flight per lane
+constexpr int kNormUnroll = 8;    // 16-byte loads in flight per lane, first pass
+constexpr int kApplyUnroll = 4;   // the same in RMSNorm's second pass
+
+template <bool NT>
+static __device__ __forceinline__ u32x4 load16(const u32x4* a) {
+  if constexpr (NT) return __builtin_nontemporal_load(a);
+  else return *a;
+}
 
 template <typename T> struct Vec;
 template <> struct Vec<_Float16> {
@@ -142,7 +154,7 @@ struct RmsState {
   }
 };
 
-template <typename T, typename S>
+template <typename T, bool NT, typename S>
 __device__ __forceinline__ void fold_chunk(const NormParams& p, int n, int c, S& st) {
   constexpr int VN = Vec<T>::N;
   // This chunk's vectors.
@@ -153,7 +165,7 @@ __device__ __forceinline__ void fold_chunk(const NormParams& p, int n, int c, S&
   for (; v + (kNormUnroll - 1) * kNormThreads < v1; v += kNormUnroll * kNormThreads) {
     u32x4 w[kNormUnroll];
 #pragma unroll
-    for (int u = 0; u < kNormUnroll; ++u) w[u] = row[v + u * kNormThreads];
+    for (int u = 0; u < kNormUnroll; ++u) w[u] = load16<NT>(row + v + u * kNormThreads);
 #pragma unroll
     for (int u = 0; u < kNormUnroll; ++u) {
       float f[VN];
@@ -163,7 +175,7 @@ __device__ __forceinline__ void fold_chunk(const NormParams& p, int n, int c, S&
   }
   for (; v < v1; v += kNormThreads) {
     float f[VN];
-    Vec<T>::load(row[v], f);
+    Vec<T>::load(load16<NT>(row + v), f);
     st.template fold<VN>(f, p.invM, p.eps);
   }
 }
@@ -194,7 +206,7 @@ template <typename T, bool RMS>
 __global__ __launch_bounds__(kNormThreads) void norm_split_kernel(NormParams p) {
   const int c = blockIdx.x % p.chunks, n = blockIdx.x / p.chunks;
   typename std::conditional<RMS, RmsState, L2State>::type st;
-  fold_chunk<T>(p, n, c, st);
+  fold_chunk<T, !RMS>(p, n, c, st);
   block_merge(st, p.eps);
   if (threadIdx.x == 0) {
     p.ws_r[blockIdx.x] = st.r;
@@ -238,13 +250,22 @@ __global__ __launch_bounds__(kNormThreads) void rms_apply_kernel(NormParams p) {
   const int v1 = (int)(min((long long)(c + 1) * p.chunk, (long long)p.M) / VN);
   const u32x4* row = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.x) + (size_t)n * p.M);
   u32x4* yrow = reinterpret_cast<u32x4*>(reinterpret_cast<T*>(p.y) + (size_t)n * p.M);
-  for (int v = v0 + threadIdx.x; v < v1; v += kNormThreads) {
+  auto scale = [&](u32x4 w) {
     float f[VN];
-    Vec<T>::load(row[v], f);
+    Vec<T>::load(w, f);
 #pragma unroll
     for (int k = 0; k < VN; ++k) f[k] *= q;
-    yrow[v] = Vec<T>::store(f);
+    return Vec<T>::store(f);
+  };
+  int v = v0 + threadIdx.x;
+  for (; v + (kApplyUnroll - 1) * kNormThreads < v1; v += kApplyUnroll * kNormThreads) {
+    u32x4 w[kApplyUnroll];
+#pragma unroll
+    for (int u = 0; u < kApplyUnroll; ++u) w[u] = load16<true>(row + v + u * kNormThreads);
+#pragma unroll
+    for (int u = 0; u < kApplyUnroll; ++u) __builtin_nontemporal_store(scale(w[u]), yrow + v + u * kNormThreads);
   }
+  for (; v < v1; v += kNormThreads) __builtin_nontemporal_store(scale(load16<true>(row + v)), yrow + v);
 }
 
 template <typename T>
