@@ -6,7 +6,7 @@
 A step is one call of the library on one batch of a workload: attn_fwd(_mod)
 for a prefill workload (one kernel), attn_decode(_mod) for a decode workload
 (split kernel + combine kernel), norm_l2 / rmsnorm_rowmax for a row reduction
-(split kernel + combine kernel).  W untimed steps, then K steps timed with HIP
+(one kernel per row, or split kernel + combine kernel).  W untimed steps, then K steps timed with HIP
 events recorded on the stream the kernels are launched on (the current torch
 stream, which the binding passes to the library), bracketed by device
 synchronisation; `ms_per_step` is their mean.  K more steps, each between
@@ -251,11 +251,8 @@ def run_norm(name, steps, warmup, *, chunks=0, errors=False):
 
     w = NORM_WORKLOADS[name]
     x = make_norm_input(w, device="cuda")
-    C = chunks or pa.norm_chunks(w.N, w.M, x.dtype)
-    if w.op == "l2":
-        kernels = [f"norm_split_kernel<{w.dtype},0>", "l2_combine_kernel"]
-    else:
-        kernels = [f"norm_split_kernel<{w.dtype},1>", f"rms_apply_kernel<{w.dtype}>"]
+    C = chunks or pa.norm_chunks(w.op, w.N, w.M, x.dtype)
+    kernels = pa.norm_kernels(w.op, w.M, x.dtype, C)
     ws = torch.empty(pa.norm_workspace_bytes(w.N, C), dtype=torch.uint8, device="cuda")
     out = torch.empty(w.N, dtype=torch.float32, device="cuda")
     xs = [x] + [x.clone() for _ in range(input_copies(x.numel() * x.element_size()) - 1)]

@@ -45,11 +45,26 @@ typedef enum {
 } norm_dtype;
 
 /*
- * Chunks per row that the library uses when `chunks` is 0 (about 512
- * workgroups in all, chunks of at least 4096 elements).  Returns >= 1, or 0
- * for invalid sizes.
+ * Chunks per row that norm_l2 (rms = 0) or rmsnorm_rowmax (rms != 0) uses
+ * when `chunks` is 0: 1 when the N rows fill at least 85 % of ceil(N / CUs)
+ * rounds of the current device's compute units (so N >= CUs) and, for
+ * RMSNorm, a row has at most 256 KiB (M * element size <= 262144): one
+ * workgroup per row, RMSNorm reading X once.  Otherwise about 512 workgroups
+ * in all with chunks of at least 4096 elements.  Without a device the CU
+ * count is taken as 256.  Returns >= 1, or 0 for invalid sizes.
  */
-int norm_chunks(int N, int M, norm_dtype dtype);
+int norm_chunks(int rms, int N, int M, norm_dtype dtype);
+
+/*
+ * The kernels that norm_l2 (rms = 0) or rmsnorm_rowmax (rms != 0) launches
+ * for rows of M elements and `chunks` (>= 1) chunks per row, written to buf
+ * as a NUL-terminated string: "l2_row_kernel<T>" or "rms_row_kernel<T>" for
+ * one kernel per row, else "norm_split_kernel<T,rms>;l2_combine_kernel" or
+ * "norm_split_kernel<T,1>;rms_apply_kernel<T>" (T = f16, bf16 or f32).
+ * Host only: no HIP call.  Errors: ATTN_ERR_UNSUPPORTED for the dtype,
+ * ATTN_ERR_SHAPE for M or chunks, or if buf is NULL or shorter than the names.
+ */
+int norm_kernels(int rms, int M, norm_dtype dtype, int chunks, char* buf, size_t len);
 
 /*
  * Workspace bytes for (N, chunks): two fp32 partials per (row, chunk), laid
@@ -65,7 +80,8 @@ size_t norm_workspace_bytes(int N, int chunks);
  * out[n] = L2 norm of row n (fp32), for n < N.  chunks >= 1, or 0 for the
  * heuristic; the chunk size is ceil(M / chunks) rounded up to whole 16-byte
  * vectors, so trailing chunks may be short or empty.  Two kernels run: the
- * chunk partials, then the per-row combine.
+ * chunk partials, then the per-row combine; with one chunk per row, one
+ * kernel (a workgroup per row writes the row's partial and its norm).
  */
 int norm_l2(const void* X, float* out, int N, int M, norm_dtype dtype, int chunks,
             void* workspace, size_t workspace_bytes, hipStream_t stream);
@@ -74,7 +90,10 @@ int norm_l2(const void* X, float* out, int N, int M, norm_dtype dtype, int chunk
  * Y [N, M] (norm_dtype, rounded to nearest even) = RMSNorm of X without a
  * weight, and rowmax[n] (fp32) = max of row n of the unrounded Y.  eps >= 0,
  * finite.  Two kernels run: the statistics of every chunk in one pass over
- * X, then a kernel that combines each row's partials and writes Y.
+ * X, then a kernel that combines each row's partials and writes Y.  With one
+ * chunk per row and rows of at most 256 KiB, one kernel runs instead: a
+ * workgroup per row holds the row in registers, writes the row's partial and
+ * its row max, and writes Y from the registers (X is read once).
  */
 int rmsnorm_rowmax(const void* X, void* Y, float* rowmax, int N, int M, float eps, norm_dtype dtype,
                    int chunks, void* workspace, size_t workspace_bytes, hipStream_t stream);

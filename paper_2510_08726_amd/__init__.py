@@ -17,7 +17,7 @@ import torch
 __all__ = [
     "attn_fwd", "attn_fwd_mod", "attn_decode", "attn_decode_mod", "attn_decode_workspace_bytes",
     "attn_decode_num_splits", "attn_decode_noalloc", "peaks_hbm_read", "peaks_mfma", "peaks_mfma_waves",
-    "peaks_mfma_operand_bytes", "norm_chunks", "norm_workspace_bytes", "norm_l2", "rmsnorm_rowmax", "attn_fwd_kernels", "attn_decode_kernels",
+    "peaks_mfma_operand_bytes", "norm_chunks", "norm_kernels", "norm_workspace_bytes", "norm_l2", "rmsnorm_rowmax", "attn_fwd_kernels", "attn_decode_kernels",
     "attn_status_string", "attn_last_hip_error", "library_path", "load_library", "AttnError",
     "ATTN_OK", "ATTN_ERR_NULL", "ATTN_ERR_SHAPE", "ATTN_ERR_UNSUPPORTED", "ATTN_ERR_WORKSPACE",
     "ATTN_ERR_HIP",
@@ -80,6 +80,8 @@ def load_library():
     lib.attn_fwd_kernels.restype = ci
     lib.attn_decode_kernels.argtypes = [ci, ci, ci, ci, ci, cf, ctypes.c_char_p, cs]
     lib.attn_decode_kernels.restype = ci
+    lib.norm_kernels.argtypes = [ci, ci, ci, ci, ctypes.c_char_p, cs]
+    lib.norm_kernels.restype = ci
     lib.peaks_hbm_read.argtypes = [vp, cs, vp, vp]
     lib.peaks_hbm_read.restype = ci
     lib.peaks_hbm_read_sink_floats.argtypes = []
@@ -90,7 +92,7 @@ def load_library():
     lib.peaks_mfma_waves.restype = ci
     lib.peaks_mfma_operand_bytes.argtypes = []
     lib.peaks_mfma_operand_bytes.restype = cs
-    lib.norm_chunks.argtypes = [ci, ci, ci]
+    lib.norm_chunks.argtypes = [ci, ci, ci, ci]
     lib.norm_chunks.restype = ci
     lib.norm_workspace_bytes.argtypes = [ci, ci]
     lib.norm_workspace_bytes.restype = cs
@@ -334,20 +336,29 @@ NORM_F16, NORM_BF16, NORM_F32 = 0, 1, 2
 _NORM_CODE = {torch.float16: NORM_F16, torch.bfloat16: NORM_BF16, torch.float32: NORM_F32}
 
 
-def norm_chunks(N, M, dtype):
-    return load_library().norm_chunks(N, M, _NORM_CODE[dtype])
+def norm_chunks(op, N, M, dtype):
+    """Chunks per row that norm_l2 (op "l2") or rmsnorm_rowmax (op "rms") uses for chunks=0."""
+    return load_library().norm_chunks(int(op == "rms"), N, M, _NORM_CODE[dtype])
+
+
+def norm_kernels(op, M, dtype, chunks):
+    """Names of the kernels norm_l2 (op "l2") or rmsnorm_rowmax (op "rms")
+    launches for rows of M elements and `chunks` >= 1 chunks per row (host only)."""
+    buf = ctypes.create_string_buffer(128)
+    _check(load_library().norm_kernels(int(op == "rms"), int(M), _NORM_CODE.get(dtype, dtype), int(chunks), buf, 128))
+    return buf.value.decode().split(";")
 
 
 def norm_workspace_bytes(N, chunks):
     return load_library().norm_workspace_bytes(N, chunks)
 
 
-def _norm_args(x, chunks, workspace):
+def _norm_args(op, x, chunks, workspace):
     _require(x.is_cuda and x.is_contiguous() and x.dim() == 2, "x must be a contiguous 2-D GPU tensor [N, M]")
     _require(x.dtype in _NORM_CODE, "x must be float16, bfloat16 or float32")
     N, M = x.shape
     lib = load_library()
-    C = chunks or lib.norm_chunks(N, M, _NORM_CODE[x.dtype])
+    C = chunks or lib.norm_chunks(int(op == "rms"), N, M, _NORM_CODE[x.dtype])
     if workspace is None:
         workspace = torch.empty(max(lib.norm_workspace_bytes(N, max(C, 1)), 16), dtype=torch.uint8,
                                 device=x.device)
@@ -356,7 +367,7 @@ def _norm_args(x, chunks, workspace):
 
 def norm_l2(x, out=None, *, chunks=0, workspace=None, stream=None):
     """Row L2 norms of x [N, M] (single pass, split over the row): out [N] float32."""
-    N, M, workspace = _norm_args(x, chunks, workspace)
+    N, M, workspace = _norm_args("l2", x, chunks, workspace)
     if out is None:
         out = torch.empty(N, dtype=torch.float32, device=x.device)
     _require(out.is_cuda and out.dtype == torch.float32 and out.numel() == N, "out must be float32 [N]")
@@ -367,7 +378,7 @@ def norm_l2(x, out=None, *, chunks=0, workspace=None, stream=None):
 
 def rmsnorm_rowmax(x, y=None, rowmax=None, *, eps=1e-6, chunks=0, workspace=None, stream=None):
     """y = x / sqrt(mean(x^2) + eps) (x's dtype) and rowmax [N] = max of each row of y (float32)."""
-    N, M, workspace = _norm_args(x, chunks, workspace)
+    N, M, workspace = _norm_args("rms", x, chunks, workspace)
     if y is None:
         y = torch.empty_like(x)
     if rowmax is None:

@@ -294,16 +294,40 @@ int peaks_mfma_waves(void) { return attn::mfma_loop_waves(); }
 
 size_t peaks_mfma_operand_bytes(void) { return attn::mfma_loop_operand_bytes(); }
 
-int norm_chunks(int N, int M, norm_dtype dtype) {
+int norm_chunks(int rms, int N, int M, norm_dtype dtype) {
   if (N < 1 || M < 1 || (dtype != NORM_F16 && dtype != NORM_BF16 && dtype != NORM_F32)) return 0;
-  // About two workgroups per compute unit (measured on the 256 x 2^17 row
-  // reductions: 2 chunks per row beat 4, 8 and 16), chunks of at least 4096
-  // elements.
+  // One chunk per row (one kernel, a workgroup per row) when the rows fill at
+  // least 85 % of the compute units' rounds and, for RMSNorm, a row fits the
+  // workgroup's registers (X is then read once; that workgroup takes a whole
+  // compute unit).  On the 256 x 2^17 workloads, from HBM: the one-pass
+  // RMSNorm ran 1.19x the two kernels with 2 chunks, the L2 norm's one-chunk
+  // kernel 1.03x its two chunks.
+  const int64_t elem = dtype == NORM_F32 ? 4 : 2, cu = compute_units();
+  const int64_t rounds = (N + cu - 1) / cu;
+  if (attn::norm_one_kernel(rms != 0, M, (int)elem, 1) && N >= cu && (int64_t)N * 100 >= rounds * cu * 85) return 1;
+  // Otherwise about two workgroups per compute unit (measured on the 256 x
+  // 2^17 row reductions: 2 chunks per row beat 4, 8 and 16), chunks of at
+  // least 4096 elements.
   constexpr int kTargetBlocks = 512, kMinChunk = 4096;
   int64_t c = (kTargetBlocks + N - 1) / N;
   const int64_t cmax = ((int64_t)M + kMinChunk - 1) / kMinChunk;
   if (c > cmax) c = cmax;
   return c < 1 ? 1 : (int)c;
+}
+
+int norm_kernels(int rms, int M, norm_dtype dtype, int chunks, char* buf, size_t len) {
+  if (dtype != NORM_F16 && dtype != NORM_BF16 && dtype != NORM_F32) return ATTN_ERR_UNSUPPORTED;
+  const int elem = dtype == NORM_F32 ? 4 : 2;
+  if (M < 1 || M % (16 / elem) || chunks < 1) return ATTN_ERR_SHAPE;
+  const char* t = dtype == NORM_F32 ? "f32" : dtype == NORM_BF16 ? "bf16" : "f16";
+  char s[96];
+  if (attn::norm_one_kernel(rms != 0, M, elem, chunks))
+    std::snprintf(s, sizeof s, "%s_row_kernel<%s>", rms ? "rms" : "l2", t);
+  else if (rms)
+    std::snprintf(s, sizeof s, "norm_split_kernel<%s,1>;rms_apply_kernel<%s>", t, t);
+  else
+    std::snprintf(s, sizeof s, "norm_split_kernel<%s,0>;l2_combine_kernel", t);
+  return put(buf, len, s);
 }
 
 size_t norm_workspace_bytes(int N, int chunks) {
@@ -323,7 +347,7 @@ int norm_run(const void* X, void* Y, float* out, int N, int M, float eps, norm_d
   const int vec = dtype == NORM_F32 ? 4 : 8;
   if (N < 1 || M < 1 || M % vec || chunks < 0 || !std::isfinite(eps) || eps < 0.f) return ATTN_ERR_SHAPE;
   if ((int64_t)N * M >= (int64_t(1) << 40)) return ATTN_ERR_SHAPE;
-  const int C = chunks ? chunks : norm_chunks(N, M, dtype);
+  const int C = chunks ? chunks : norm_chunks(rms ? 1 : 0, N, M, dtype);
   if ((int64_t)N * C > kMaxGrid) return ATTN_ERR_SHAPE;
   if (workspace_bytes < norm_workspace_bytes(N, C) || (reinterpret_cast<uintptr_t>(workspace) & 15))
     return ATTN_ERR_WORKSPACE;

@@ -99,6 +99,15 @@ struct NormParams {
   float invM;           // 1 / M
 };
 hipError_t launch_norm(const NormParams& p, hipStream_t stream);
+// Longest row (bytes) that RMSNorm with one chunk per row holds in the
+// registers of one workgroup (1024 lanes x 16 vectors of 16 bytes), reading X once.
+constexpr long long kNormRowBytes = 1024LL * 16 * 16;
+// True when a row reduction with `chunks` chunks per row runs one kernel
+// (one workgroup per row: the L2 norm always, RMSNorm when the row fits)
+// rather than the chunk partials and a second kernel.
+inline bool norm_one_kernel(bool rms, long long M, int elem, int chunks) {
+  return chunks == 1 && (!rms || M * elem <= kNormRowBytes);
+}
 
 // Achievable-peak probes (peaks.hip).
 hipError_t launch_hbm_read(const void* buf, size_t bytes, float* sink, hipStream_t stream);

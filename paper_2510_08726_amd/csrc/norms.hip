@@ -3,14 +3,17 @@
 // second workload; see include/norms.h).  Both are HBM streams: every lane
 // reads 16-byte vectors of its row chunk, folds each vector into its state
 // with one repaired update (the vector's own max and sum first, the
-// privatised local reduction), the 256 lanes' states are combined with the
-// same repair, and the chunk partials of a row are combined by the second
-// kernel.
+// privatised local reduction), the lanes' states are combined with the same
+// repair, and the chunk partials of a row are combined by a second kernel.
+// With one chunk per row the combine is the workgroup's own: the L2 norm
+// writes the norm from the first kernel, and RMSNorm, when the row fits in
+// the workgroup's registers, writes y from them without reading X again.
 //
-// Cache policy: X is read once by the L2 norm and last by RMSNorm's second
-// kernel, so those loads (and the stores of y) are nontemporal; RMSNorm's
-// first pass reads X with ordinary loads so that the second pass finds what
-// the caches (L2 and the memory-side cache) still hold of it.
+// Cache policy: X is read once by the L2 norm and by the one-pass RMSNorm,
+// and last by RMSNorm's second kernel, so those loads (and the stores of y)
+// are nontemporal; RMSNorm's first pass reads X with ordinary loads so that
+// the second pass finds what the caches (L2 and the memory-side cache) still
+// hold of it.
 
 #include <type_traits>
 
@@ -22,6 +25,9 @@ namespace attn {
 namespace {
 
 constexpr int kNormThreads = 256;
+constexpr int kL2RowThreads = 512;   // the L2 norm with one chunk per row
+constexpr int kRowThreads = 1024;    // the one-pass RMSNorm: one row per workgroup
+constexpr int kRowVecs = (int)(kNormRowBytes / (kRowThreads * 16));   // 16-byte vectors per lane
 constexpr int kNormUnroll = 8;    // 16-byte loads in flight per lane, first pass
 constexpr int kApplyUnroll = 4;   // the same in RMSNorm's second pass
 
@@ -154,7 +160,7 @@ struct RmsState {
   }
 };
 
-template <typename T, bool NT, typename S>
+template <typename T, bool NT, int NTH, typename S>
 __device__ __forceinline__ void fold_chunk(const NormParams& p, int n, int c, S& st) {
   constexpr int VN = Vec<T>::N;
   // This chunk's vectors.
@@ -162,10 +168,10 @@ __device__ __forceinline__ void fold_chunk(const NormParams& p, int n, int c, S&
   const int v1 = (int)(min((long long)(c + 1) * p.chunk, (long long)p.M) / VN);
   const u32x4* row = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.x) + (size_t)n * p.M);
   int v = v0 + threadIdx.x;
-  for (; v + (kNormUnroll - 1) * kNormThreads < v1; v += kNormUnroll * kNormThreads) {
+  for (; v + (kNormUnroll - 1) * NTH < v1; v += kNormUnroll * NTH) {
     u32x4 w[kNormUnroll];
 #pragma unroll
-    for (int u = 0; u < kNormUnroll; ++u) w[u] = load16<NT>(row + v + u * kNormThreads);
+    for (int u = 0; u < kNormUnroll; ++u) w[u] = load16<NT>(row + v + u * NTH);
 #pragma unroll
     for (int u = 0; u < kNormUnroll; ++u) {
       float f[VN];
@@ -173,18 +179,18 @@ __device__ __forceinline__ void fold_chunk(const NormParams& p, int n, int c, S&
       st.template fold<VN>(f, p.invM, p.eps);
     }
   }
-  for (; v < v1; v += kNormThreads) {
+  for (; v < v1; v += NTH) {
     float f[VN];
     Vec<T>::load(load16<NT>(row + v), f);
     st.template fold<VN>(f, p.invM, p.eps);
   }
 }
 
-// Combine the states of the workgroup's 256 lanes (the same repaired merge),
+// Combine the states of the workgroup's NTH lanes (the same repaired merge),
 // leaving the result in lane 0 of wave 0.
-template <typename S>
+template <int NTH, typename S>
 __device__ __forceinline__ void block_merge(S& st, float eps) {
-  __shared__ float sr[kNormThreads / 64], stt[kNormThreads / 64];
+  __shared__ float sr[NTH / 64], stt[NTH / 64];
 #pragma unroll
   for (int x = 32; x >= 1; x >>= 1) {
     const float r2 = __shfl_xor(st.r, x, 64), t2 = __shfl_xor(st.t, x, 64);
@@ -197,7 +203,7 @@ __device__ __forceinline__ void block_merge(S& st, float eps) {
   __syncthreads();
   if (threadIdx.x == 0) {
 #pragma unroll
-    for (int w = 1; w < kNormThreads / 64; ++w) st.merge(sr[w], stt[w], eps);
+    for (int w = 1; w < NTH / 64; ++w) st.merge(sr[w], stt[w], eps);
   }
 }
 
@@ -206,11 +212,26 @@ template <typename T, bool RMS>
 __global__ __launch_bounds__(kNormThreads) void norm_split_kernel(NormParams p) {
   const int c = blockIdx.x % p.chunks, n = blockIdx.x / p.chunks;
   typename std::conditional<RMS, RmsState, L2State>::type st;
-  fold_chunk<T, !RMS>(p, n, c, st);
-  block_merge(st, p.eps);
+  fold_chunk<T, !RMS, kNormThreads>(p, n, c, st);
+  block_merge<kNormThreads>(st, p.eps);
   if (threadIdx.x == 0) {
     p.ws_r[blockIdx.x] = st.r;
     p.ws_t[blockIdx.x] = st.t;
+  }
+}
+
+// The L2 norm with one chunk per row: one workgroup of 512 lanes per row
+// writes the row's partial and its norm.
+template <typename T>
+__global__ __launch_bounds__(kL2RowThreads) void l2_row_kernel(NormParams p) {
+  const int n = blockIdx.x;
+  L2State st;
+  fold_chunk<T, true, kL2RowThreads>(p, n, 0, st);
+  block_merge<kL2RowThreads>(st, 0.f);
+  if (threadIdx.x == 0) {
+    p.ws_r[n] = st.r;
+    p.ws_t[n] = st.t;
+    p.out[n] = st.r * __builtin_sqrtf(st.t);
   }
 }
 
@@ -268,9 +289,69 @@ __global__ __launch_bounds__(kNormThreads) void rms_apply_kernel(NormParams p) {
   for (; v < v1; v += kNormThreads) __builtin_nontemporal_store(scale(load16<true>(row + v)), yrow + v);
 }
 
+// One-pass RMSNorm, one workgroup per row of at most kRowThreads x kRowVecs
+// vectors: every lane loads its vectors of the row (all loads in flight at
+// once) and keeps them in registers, folds them into its state, the lanes'
+// states are merged (the row's statistics, written as its one partial and
+// its row max), and y is written from the registers.
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void rms_row_kernel(NormParams p) {
+  constexpr int VN = Vec<T>::N;
+  const int n = blockIdx.x;
+  const int nv = p.M / VN;
+  const u32x4* row = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.x) + (size_t)n * p.M);
+  u32x4* yrow = reinterpret_cast<u32x4*>(reinterpret_cast<T*>(p.y) + (size_t)n * p.M);
+  u32x4 w[kRowVecs];
+#pragma unroll
+  for (int u = 0; u < kRowVecs; ++u) {
+    const int v = threadIdx.x + u * kRowThreads;
+    w[u] = v < nv ? load16<true>(row + v) : u32x4{0u, 0u, 0u, 0u};
+  }
+  RmsState st;
+#pragma unroll
+  for (int u = 0; u < kRowVecs; ++u) {
+    if (threadIdx.x + u * kRowThreads < nv) {
+      float f[VN];
+      Vec<T>::load(w[u], f);
+      st.template fold<VN>(f, p.invM, p.eps);
+    }
+    // Keep the loaded words, not their conversions, live until the stores
+    // (half the registers for fp16 and bf16).
+    asm volatile("" : "+v"(w[u]));
+  }
+  block_merge<kRowThreads>(st, p.eps);
+  __shared__ float s_q;
+  if (threadIdx.x == 0) {
+    p.ws_r[n] = st.r;
+    p.ws_t[n] = st.t;
+    p.out[n] = st.t;
+    s_q = 1.f / __builtin_sqrtf(st.r + p.eps);
+  }
+  __syncthreads();
+  const float q = s_q;
+#pragma unroll
+  for (int u = 0; u < kRowVecs; ++u) {
+    const int v = threadIdx.x + u * kRowThreads;
+    if (v < nv) {
+      float f[VN];
+      Vec<T>::load(w[u], f);
+#pragma unroll
+      for (int k = 0; k < VN; ++k) f[k] *= q;
+      __builtin_nontemporal_store(Vec<T>::store(f), yrow + v);
+    }
+  }
+}
+
 template <typename T>
 hipError_t launch_norm_t(const NormParams& p, hipStream_t stream) {
   const dim3 grid(p.N * p.chunks), block(kNormThreads);
+  if (norm_one_kernel(p.rms != 0, p.M, (int)sizeof(T), p.chunks)) {
+    if (p.rms)
+      hipLaunchKernelGGL((rms_row_kernel<T>), grid, dim3(kRowThreads), 0, stream, p);
+    else
+      hipLaunchKernelGGL((l2_row_kernel<T>), grid, dim3(kL2RowThreads), 0, stream, p);
+    return hipGetLastError();
+  }
   if (p.rms) {
     hipLaunchKernelGGL((norm_split_kernel<T, true>), grid, block, 0, stream, p);
     hipError_t e = hipGetLastError();

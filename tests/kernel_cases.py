@@ -3,7 +3,8 @@
 ``tests/test_kernel_coverage.py`` (CPU) checks that the kernels these cases
 dispatch to, as named by the library's own dispatch (attn_fwd_kernels /
 attn_decode_kernels), are exactly the kernels in the build;
-``tests/test_gpu_variants.py`` runs every case on the GPU against the oracle.
+``tests/test_gpu_variants.py`` runs every case on the GPU against the oracle,
+``tests/test_gpu_norms.py`` every row-reduction case (both operations).
 """
 
 # Prefill: (B, Hq, Hkv, Lq, Lk, D, dtype, causal, alibi, softcap, window).
@@ -40,6 +41,28 @@ for _D in (64, 128):
                 for _cap in (None, 2.0):
                     _Lk = 333 + 50 * len(DECODE_VARIANT_CASES) % 400
                     DECODE_VARIANT_CASES.append((1, _Hq, _Hkv, _Lk, _D, _dt, _a, _cap, 3))
+
+
+# Row reductions: (N, M, dtype, chunks), chunks 0 for the library's choice.
+# Every dtype has cases with several chunks per row (chunk partials and a
+# second kernel) and with one (a workgroup per row); RMSNorm's one-pass
+# kernel at its longest row and one vector past it (then the two kernels run
+# with one chunk).
+NORM_CASES = [
+    (3, 8, "f16", 0),            # one vector per row
+    (32, 1024, "bf16", 0),       # the smallest paper shape
+    (7, 1000, "f16", 3),         # chunks of 336 elements: the last one short
+    (5, 4104, "bf16", 5),        # ragged chunk ends
+    (2, 64, "f16", 40),          # more chunks than vectors: empty chunks
+    (9, 3000, "f32", 4),
+    (4, 4, "f32", 0),
+    (64, 1 << 15, "bf16", 0),
+    (5, 1000, "f16", 1),         # one chunk: 125 vectors, most lanes idle
+    (3, 1 << 17, "bf16", 1),     # the longest row held in registers: 16 vectors every lane
+    (2, 1 << 16, "f32", 1),      # the same in fp32
+    (2, (1 << 17) + 8, "bf16", 1),   # one vector longer: RMSNorm's two kernels, one chunk
+    (300, 2048, "f16", 1),       # more rows than compute units
+]
 
 
 def case_id(c):

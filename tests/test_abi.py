@@ -46,15 +46,39 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_norm_chunk_heuristic(lib):
-    """Host logic of the row reductions' split: about 512 workgroups with
-    chunks of >= 4096 elements."""
+    """Host logic of the row reductions' split (no device here: 256 compute
+    units): one chunk per row when the rows fill >= 85 % of the compute
+    units' rounds (for RMSNorm, rows of <= 256 KiB), else about 512
+    workgroups with chunks of >= 4096 elements."""
     F16, BF16, F32 = 0, 1, 2
-    assert lib.norm_chunks(256, 1 << 17, F32) == 2
-    assert lib.norm_chunks(256, 1 << 17, BF16) == 2
-    assert lib.norm_chunks(32, 1 << 10, F16) == 1           # chunks of >= 4096 elements
-    assert lib.norm_chunks(32, 1 << 17, F16) == 16          # 512 workgroups
-    assert lib.norm_chunks(1, 40000, BF16) == 10            # 512 / N, capped by M / 4096
-    assert lib.norm_chunks(0, 8, F16) == 0 and lib.norm_chunks(8, 8, 7) == 0
+    for rms in (0, 1):
+        assert lib.norm_chunks(rms, 256, 1 << 17, BF16) == 1     # 256 KiB rows, one round of 256
+        assert lib.norm_chunks(rms, 512, 1 << 16, F32) == 1
+        assert lib.norm_chunks(rms, 480, 4096, F16) == 1         # 480 of 512 slots: 94 %
+        assert lib.norm_chunks(rms, 300, 1 << 17, BF16) == 2     # 300 of 512 slots: 512 / N
+        assert lib.norm_chunks(rms, 255, 1 << 17, BF16) == 3     # fewer rows than compute units
+        assert lib.norm_chunks(rms, 32, 1 << 10, F16) == 1       # chunks of >= 4096 elements
+        assert lib.norm_chunks(rms, 32, 1 << 17, F16) == 16      # 512 workgroups
+        assert lib.norm_chunks(rms, 1, 40000, BF16) == 10        # 512 / N, capped by M / 4096
+        assert lib.norm_chunks(rms, 0, 8, F16) == 0 and lib.norm_chunks(rms, 8, 8, 7) == 0
+    assert lib.norm_chunks(0, 256, 1 << 17, F32) == 1            # the L2 norm: any row length
+    assert lib.norm_chunks(1, 256, 1 << 17, F32) == 2            # RMSNorm: a 512 KiB row
+
+
+def test_norm_kernel_query():
+    """The kernels each row-reduction path launches (host only)."""
+    import torch
+    f16, bf16, f32 = torch.float16, torch.bfloat16, torch.float32
+    assert pa.norm_kernels("l2", 1 << 17, f32, 2) == ["norm_split_kernel<f32,0>", "l2_combine_kernel"]
+    assert pa.norm_kernels("rms", 1 << 17, bf16, 2) == ["norm_split_kernel<bf16,1>", "rms_apply_kernel<bf16>"]
+    assert pa.norm_kernels("l2", 1 << 20, f16, 1) == ["l2_row_kernel<f16>"]          # any row length
+    assert pa.norm_kernels("rms", 1 << 17, bf16, 1) == ["rms_row_kernel<bf16>"]      # 256 KiB: held in registers
+    assert pa.norm_kernels("rms", 1 << 16, f32, 1) == ["rms_row_kernel<f32>"]
+    assert pa.norm_kernels("rms", (1 << 17) + 8, bf16, 1) == ["norm_split_kernel<bf16,1>", "rms_apply_kernel<bf16>"]
+    assert pa.norm_kernels("rms", (1 << 16) + 4, f32, 1) == ["norm_split_kernel<f32,1>", "rms_apply_kernel<f32>"]
+    for bad in ((1 << 17, bf16, 0), (1001, f16, 1), (0, f16, 1)):
+        with pytest.raises(pa.AttnError):
+            pa.norm_kernels("rms", *bad)
 
 
 def test_status_strings(lib):

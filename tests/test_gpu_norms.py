@@ -10,6 +10,7 @@ import torch
 import paper_2510_08726_amd as pa
 from oracle import norms
 from paper_2510_08726_amd.workloads import NORM_DTYPES, NORM_WORKLOADS, make_norm_input, NormWorkload
+from kernel_cases import NORM_CASES as CASES
 
 pytestmark = pytest.mark.gpu
 
@@ -17,18 +18,6 @@ pytestmark = pytest.mark.gpu
 RTOL_STAT = 2e-5
 # y is rounded to the input type: half an ulp, relative.
 RTOL_Y = {"f16": 2.0 ** -11, "bf16": 2.0 ** -8, "f32": 2e-6}
-
-CASES = [  # N, M, dtype, chunks
-    (3, 8, "f16", 0),          # one vector per row
-    (32, 1024, "bf16", 0),     # the smallest paper shape
-    (7, 1000, "f16", 3),       # chunks of 336 elements: the last one short
-    (5, 4104, "bf16", 5),      # ragged chunk ends
-    (2, 64, "f16", 40),        # more chunks than vectors: empty chunks
-    (9, 3000, "f32", 4),
-    (4, 4, "f32", 0),
-    (64, 1 << 15, "bf16", 0),
-]
-
 
 def _x(N, M, dt, seed):
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -47,7 +36,7 @@ def test_l2_norm_matches_oracle(case):
     print(f"l2 norm case {case}", flush=True)
     x = _x(N, M, dt, 300 + N)
     xd = x.cuda()
-    Cres = C or pa.norm_chunks(N, M, x.dtype)
+    Cres = C or pa.norm_chunks("l2", N, M, x.dtype)
     ws = torch.empty(pa.norm_workspace_bytes(N, Cres), dtype=torch.uint8, device="cuda")
     out = pa.norm_l2(xd, chunks=C, workspace=ws)
     torch.cuda.synchronize()
@@ -67,7 +56,7 @@ def test_rmsnorm_rowmax_matches_oracle(case):
     eps = 1e-5
     x = _x(N, M, dt, 400 + N)
     xd = x.cuda()
-    Cres = C or pa.norm_chunks(N, M, x.dtype)
+    Cres = C or pa.norm_chunks("rms", N, M, x.dtype)
     ws = torch.empty(pa.norm_workspace_bytes(N, Cres), dtype=torch.uint8, device="cuda")
     y, m = pa.rmsnorm_rowmax(xd, eps=eps, chunks=C, workspace=ws)
     torch.cuda.synchronize()

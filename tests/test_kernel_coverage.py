@@ -12,7 +12,7 @@ import pytest
 
 import paper_2510_08726_amd as pa
 from paper_2510_08726_amd import build as libbuild
-from kernel_cases import DECODE_VARIANT_CASES, PREFILL_VARIANT_CASES
+from kernel_cases import DECODE_VARIANT_CASES, NORM_CASES, PREFILL_VARIANT_CASES
 
 _ARG = re.compile(r"Li(-?\d+)E|DF16_|DF16b|Lb([01])E|^f")
 
@@ -64,11 +64,11 @@ def test_every_compiled_kernel_is_exercised(compiled):
         used.update(pa.attn_fwd_kernels(D, dt[d], causal, alibi, cap or 0.0, win or 0))
     for B, Hq, Hkv, Lk, D, d, alibi, cap, S in DECODE_VARIANT_CASES:
         used.update(pa.attn_decode_kernels(Hq, Hkv, D, dt[d], alibi, cap or 0.0))
-    # the norm kernels: tests/test_gpu_norms.py runs both operations in every dtype
-    for d in ("f16", "bf16", "f32"):
-        used.update({f"norm_split_kernel<{d},0>", f"norm_split_kernel<{d},1>", f"rms_apply_kernel<{d}>"})
-    used.add("l2_combine_kernel")
-    assert len(compiled) == 32 + 64 + 16 + 4 + 10, sorted(compiled)
+    ndt = {"f16": torch.float16, "bf16": torch.bfloat16, "f32": torch.float32}
+    for N, M, d, C in NORM_CASES:   # tests/test_gpu_norms.py runs both operations on each
+        for op in ("l2", "rms"):
+            used.update(pa.norm_kernels(op, M, ndt[d], C or pa.norm_chunks(op, N, M, ndt[d])))
+    assert len(compiled) == 32 + 64 + 16 + 4 + 16, sorted(compiled)
     assert used == compiled, (sorted(compiled - used), sorted(used - compiled))
 
 
