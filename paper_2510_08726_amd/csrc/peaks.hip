@@ -9,24 +9,29 @@ namespace attn {
 namespace {
 
 constexpr int kReadThreads = 256;
-constexpr int kReadBlocks = 4096;
-constexpr int kReadUnroll = 4;   // 16-byte loads in flight per lane
+constexpr int kReadBlocks = 1024;
+constexpr int kReadUnroll = 16;   // 16-byte loads in flight per lane
 
-// Grid-stride streaming read: lane t of the grid reads 16-byte words t, t +
-// N, ... (N = threads in the grid), kReadUnroll words at a time.
+// Streaming read, one contiguous chunk per workgroup (ceil(words / grid)
+// 16-byte words): lane t of the workgroup reads words t, t + 256, ... of its
+// chunk, kReadUnroll words at a time.  (A grid-stride order, where the whole
+// grid sweeps the buffer together with 4 loads in flight a lane, measured
+// 6.16 TB/s against 7.1 for this one.)
 __global__ __launch_bounds__(kReadThreads) void hbm_read_kernel(const u32x4* __restrict__ buf, size_t words,
                                                                   float* sink) {
-  const size_t n = (size_t)gridDim.x * kReadThreads;
-  size_t i = (size_t)blockIdx.x * kReadThreads + threadIdx.x;
+  const size_t per = (words + gridDim.x - 1) / gridDim.x;
+  const size_t end = min((size_t)(blockIdx.x + 1) * per, words);
+  const size_t n = kReadThreads;
+  size_t i = min((size_t)blockIdx.x * per, words) + threadIdx.x;
   uint32_t acc = 0;
-  for (; i + (kReadUnroll - 1) * n < words; i += kReadUnroll * n) {
+  for (; i + (kReadUnroll - 1) * n < end; i += kReadUnroll * n) {
     u32x4 w[kReadUnroll];
 #pragma unroll
     for (int u = 0; u < kReadUnroll; ++u) w[u] = __builtin_nontemporal_load(buf + i + u * n);
 #pragma unroll
     for (int u = 0; u < kReadUnroll; ++u) acc ^= w[u][0] ^ w[u][1] ^ w[u][2] ^ w[u][3];
   }
-  for (; i < words; i += n) {
+  for (; i < end; i += n) {
     const u32x4 w = __builtin_nontemporal_load(buf + i);
     acc ^= w[0] ^ w[1] ^ w[2] ^ w[3];
   }
