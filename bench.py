@@ -64,7 +64,7 @@ SIDE = {
 }
 # decode split counts swept beside the library's choice: the per-head kernel
 # (MHA decode) and the grouped matrix-unit kernel (long GQA decode)
-SWEEPS = {"mha_decode": (16, 32, 64), "gqa_long_decode": (1, 2, 4, 8)}
+SWEEPS = {"mha_decode": (1, 2, 4, 8, 32), "gqa_long_decode": (1, 2, 4, 8)}
 # chunks per row swept beside the library's choice for the row reductions
 NORM_SWEEP = (1, 2, 4, 8, 16, 32)
 # input bytes that the HBM-bound workloads rotate through, 8x the memory-side cache
