@@ -51,13 +51,23 @@ def _kernels(asm):
     return out
 
 
-def test_norm_split_kernels_load_whole_vectors():
+# Kernels that read X: the 16-byte loads each issues at least (its unrolled
+# loads plus a tail load, or the 16 vectors a lane holds), and its 4-byte
+# loads (rms_apply_kernel reads the two fp32 partials of a chunk; X is never
+# read 4 bytes at a time).
+_X_READERS = {"norm_split_kernel": (9, 0), "rms_apply_kernel": (5, 2), "l2_row_kernel": (9, 0),
+              "rms_row_kernel": (16, 0)}
+
+
+def test_norm_kernels_load_whole_vectors():
     asm = os.path.join(libbuild.unit_dir("norms"), f"norms-hip-amdgcn-amd-amdhsa-{libbuild.ARCH}.s")
     if not os.path.exists(asm):
         import __graft_entry__
         __graft_entry__.build()
-    ks = {k: v for k, v in _kernels(asm).items() if "norm_split_kernel" in k}
-    assert len(ks) == 6
-    for k, ops in ks.items():
-        assert ops.count("global_load_dwordx4") >= 5, k
-        assert "global_load_dword" not in ops, k
+    kernels = _kernels(asm)
+    for name, (least, dwords) in _X_READERS.items():
+        ks = {k: v for k, v in kernels.items() if name in k}
+        assert len(ks) == (6 if name == "norm_split_kernel" else 3), name
+        for k, ops in ks.items():
+            assert ops.count("global_load_dwordx4") >= least, k
+            assert ops.count("global_load_dword") == dwords, k
