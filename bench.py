@@ -6,19 +6,20 @@
 A step is one call of the library on one batch of a workload: attn_fwd(_mod)
 for a prefill workload (one kernel), attn_decode(_mod) for a decode workload
 (split kernel + combine kernel), norm_l2 / rmsnorm_rowmax for a row reduction
-(one kernel per row, or split kernel + combine kernel).  W untimed steps, then K steps timed with HIP
-events recorded on the stream the kernels are launched on (the current torch
-stream, which the binding passes to the library), bracketed by device
-synchronisation; `ms_per_step` is their mean.  K more steps, each between
+(one kernel per row, or split kernel + combine kernel).  W untimed steps,
+continued until at least WARMUP_MS of load has passed (so that the clock has
+risen), then K steps timed with HIP events recorded on the stream the kernels
+are launched on (the current torch stream, which the binding passes to the
+library), bracketed by device synchronisation; `ms_per_step` is their mean.  K more steps, each between
 its own pair of events, give `launch_ms` (min and max per step).  All inputs
 are resident in HBM before the timed region.
 
-The HBM-bound workloads (decode, row reductions) take their inputs in turn
-from copies that span at least 2 GiB, so that no step finds its input in the
-256 MB memory-side cache (Infinity Cache) that the previous steps filled:
-their `GB/s` is the rate from HBM.  `GB/s_same_input` is the rate with one
-input read by every step, as a caller that re-reads a cache-resident tensor
-would see it.
+Every workload takes its inputs in turn from copies that span at least
+2 GiB, so that no step finds its input in the 256 MB memory-side cache
+(Infinity Cache) that the previous steps filled: the rates are those of
+inputs read from HBM.  `GB/s_same_input` / `TFLOP/s_same_input` are the
+rates with one input read by every step, as a caller that re-reads a
+cache-resident tensor would see them.
 
 The headline line is the causal MHA prefill workload (B=4, H=32, L=2048,
 D=128, fp16): `value` is its algorithmic TFLOP/s (4*D per visible query/key
@@ -67,13 +68,19 @@ SIDE = {
 SWEEPS = {"mha_decode": (1, 2, 4, 8, 32), "gqa_long_decode": (1, 2, 4, 8)}
 # chunks per row swept beside the library's choice for the row reductions
 NORM_SWEEP = (1, 2, 4, 8, 16, 32)
-# input bytes that the HBM-bound workloads rotate through, 8x the memory-side cache
+# minimum warm-up before every timing: after an idle second the GPU needs
+# about 100 steps of the causal prefill (tens of ms) to reach its clock
+# (measured: 726-734 TFLOP/s after 3 warm-up steps, 842-851 after 300)
+WARMUP_MS = 200.0
+# input bytes that the workloads rotate through, 8x the memory-side cache, in
+# at most MAX_COPIES copies (the tiny workload's inputs stay cache-sized)
 COLD_BYTES = 2 << 30
+MAX_COPIES = 32
 
 
 def input_copies(nbytes):
-    """Copies of an input of `nbytes` that span COLD_BYTES (at least 2)."""
-    return max(2, -(-COLD_BYTES // nbytes))
+    """Copies of an input of `nbytes` that span COLD_BYTES (2 to MAX_COPIES)."""
+    return max(2, min(MAX_COPIES, -(-COLD_BYTES // nbytes)))
 
 
 def kernel_source_hash(kind):
@@ -119,6 +126,8 @@ def parse():
     ap.add_argument("--splits", type=int, default=0, help="decode split count or norm chunks per row with --only (0: library)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--warmup-ms", type=float, default=WARMUP_MS,
+                    help="minimum warm-up load before every timing (0: exactly W steps, for counter passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-errors", action="store_true")
     ap.add_argument("--no-peaks", action="store_true")
@@ -131,13 +140,24 @@ def time_steps(fn, steps, warmup):
     """Mean ms per launch over `steps` back-to-back launches (HIP events on
     the launch stream around all of them), the host wall time per launch, and
     the min and max of `steps` more launches timed one by one.  `fn` is a
-    callable or a list of callables that successive steps take in turn."""
+    callable or a list of callables that successive steps take in turn.
+    Before them: `warmup` untimed steps, continued in batches until at least
+    WARMUP_MS of wall time has passed (the GPU raises its clock only after
+    tens of milliseconds of load)."""
     import torch
     fns = list(fn) if isinstance(fn, (list, tuple)) else [fn]
     n = len(fns)
-    for i in range(warmup):
+    t0 = time.perf_counter()
+    i = 0
+    for _ in range(warmup):
         fns[i % n]()
+        i += 1
     torch.cuda.synchronize()
+    while (time.perf_counter() - t0) * 1e3 < WARMUP_MS:
+        for _ in range(20):
+            fns[i % n]()
+            i += 1
+        torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
@@ -198,46 +218,48 @@ def run_workload(name, steps, warmup, *, splits=0, errors=False):
     w = WORKLOADS[name]
     q, k, v, sl = make_inputs(w, device="cuda")
     o = torch.empty_like(q)
+    in_bytes = sum(t.numel() * t.element_size() for t in (q, k, v))
+    sets = [(q, k, v)] + [(q.clone(), k.clone(), v.clone()) for _ in range(input_copies(in_bytes) - 1)]
     if w.decode:
         S = splits or w.num_splits or pa.attn_decode_num_splits(w.B, w.Hq, w.Hkv, w.Lk, w.D)
         ws = torch.empty(pa.attn_decode_workspace_bytes(w.B, w.Hq, w.D, S), dtype=torch.uint8,
                          device="cuda")
         work = decode_bytes(w.B, w.Hq, w.Hkv, w.Lk, w.D)
-        sets = [(q, k, v)] + [(q.clone(), k.clone(), v.clone()) for _ in range(input_copies(work) - 1)]
 
         def step(qs, ks, vs):
             return lambda: pa.attn_decode(qs, ks, vs, o, scale=w.sm_scale, alibi_slopes=sl,
                                           softcap=w.softcap or None, num_splits=S, workspace=ws)
-        fn = [step(*t) for t in sets]
         kernels = pa.attn_decode_kernels(w.Hq, w.Hkv, w.D, q.dtype, sl is not None, w.softcap)
     else:
         S = None
 
-        def fn():
-            pa.attn_fwd(q, k, v, o, causal=w.causal, scale=w.sm_scale, alibi_slopes=sl,
-                        softcap=w.softcap or None, window=w.window or None)
+        def step(qs, ks, vs):
+            return lambda: pa.attn_fwd(qs, ks, vs, o, causal=w.causal, scale=w.sm_scale, alibi_slopes=sl,
+                                       softcap=w.softcap or None, window=w.window or None)
         work = prefill_flops(w.B, w.Hq, w.Lq, w.Lk, w.D, w.causal, w.window)
         kernels = pa.attn_fwd_kernels(w.D, q.dtype, w.causal, sl is not None, w.softcap, w.window)
+    fn = [step(*t) for t in sets]
     ms, wall_ms, each = time_steps(fn, steps, warmup)
-    ms_same = time_steps(fn[0], steps, warmup)[0] if w.decode else None
+    # One input read by every step (the last calls: o is then set 0's output).
+    ms_same = time_steps(fn[0], steps, warmup)[0]
     res = {
         "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Lq": w.Lq, "Lk": w.Lk, "D": w.D, "dtype": w.dtype,
         "causal": w.causal, "alibi": w.alibi, "softcap": w.softcap, "window": w.window,
         "kernels": kernels, "ms_per_step": round(ms, 5), "launch_ms": each,
-        "host_wall_ms_per_step": round(wall_ms, 5),
+        "host_wall_ms_per_step": round(wall_ms, 5), "input_copies": len(sets),
     }
     if w.decode:
         gbs = work / (ms * 1e-3) / 1e9
         res.update({"num_splits": S, "bytes_per_step": work, "GB/s": round(gbs, 1),
-                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2), "input_copies": len(sets),
+                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
                     "GB/s_same_input": round(work / (ms_same * 1e-3) / 1e9, 1)})
     else:
         tf = work / (ms * 1e-3) / 1e12
         res.update({"flops_per_step": work, "TFLOP/s": round(tf, 2),
-                    "pct_mfma_peak": round(100 * tf / MFMA_PEAK_TFLOPS, 2)})
+                    "pct_mfma_peak": round(100 * tf / MFMA_PEAK_TFLOPS, 2),
+                    "TFLOP/s_same_input": round(work / (ms_same * 1e-3) / 1e12, 2)})
     err = attention_errors(w, q, k, v, sl, o) if errors else None
-    if w.decode:
-        del sets, fn
+    del sets, fn
     del q, k, v, o
     torch.cuda.empty_cache()
     return res, err
@@ -309,8 +331,10 @@ def achievable_peaks():
     iters = 20000
     for dt, key in ((torch.float16, "f16"), (torch.bfloat16, "bf16")):
         o = ops.to(dt)
-        pa.peaks_mfma(dt, 200, o)
-        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < WARMUP_MS:   # the same warm-up as every workload
+            pa.peaks_mfma(dt, iters, o)
+            torch.cuda.synchronize()
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.record()
         _, ck = pa.peaks_mfma(dt, iters, o)
@@ -323,8 +347,8 @@ def achievable_peaks():
         out[f"mfma_{key}_frac_of_spec"] = round(out[f"mfma_{key}_TFLOPs"] / MFMA_PEAK_TFLOPS, 4)
         out[f"mfma_{key}_clock_GHz"] = round(c[0] / c[1] * 0.1, 3) if c[1] else None
     out["method"] = ("peaks_hbm_read over 2 GiB (10 launches); peaks_mfma: 32x32x16 MFMAs on operands "
-                     "that change every instruction, 2 waves per SIMD, 20000 x 16 per wave; clock from "
-                     "s_memtime / s_memrealtime")
+                     "that change every instruction, 2 waves per SIMD, 20000 x 16 per wave, one launch; "
+                     f"each after at least {WARMUP_MS:.0f} ms of the same load; clock from s_memtime / s_memrealtime")
     return out
 
 
@@ -448,7 +472,9 @@ def cpu_baseline(budget_s):
 
 
 def main():
+    global WARMUP_MS
     args = parse()
+    WARMUP_MS = args.warmup_ms
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on exactly one GPU (no multi-GPU path); "
               "use --gpus 1", file=sys.stderr)
@@ -503,7 +529,7 @@ def main():
     w = WORKLOADS[HEADLINE]
     line = {
         "metric": METRIC, "value": head["TFLOP/s"], "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "steps": args.steps, "warmup": args.warmup, "warmup_min_ms": WARMUP_MS, "ms_per_step": head["ms_per_step"],
         "launch_ms": head["launch_ms"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
         "data": "synthetic",

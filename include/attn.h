@@ -137,12 +137,12 @@ size_t attn_decode_workspace_bytes(int B, int Hq, int D, int num_splits);
 
 /*
  * The number of key chunks attn_decode uses when num_splits == 0 (the library
- * heuristic).  With one query head per KV head (or more than 32): about two
- * workgroups per compute unit of the current device, chunks of at least 256
- * keys.  With 2..32 query heads per KV head, served together by one
- * workgroup per (chunk, KV head, batch): about one workgroup per compute
- * unit, chunks of at least 128 keys.  The compute units are taken as 256 if
- * the device cannot be queried.
+ * heuristic): about one workgroup per compute unit of the current device (256
+ * if it cannot be queried).  With one query head per KV head (or more than
+ * 32), one workgroup per (chunk, KV head, batch, query-head group) and
+ * chunks of at least 256 keys; with 2..32 query heads per KV head, served
+ * together by one workgroup per (chunk, KV head, batch), chunks of at least
+ * 128 keys.
  * Returns a value >= 1, or 0 for invalid sizes.
  */
 int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D);

@@ -20,7 +20,7 @@ thread_local int g_last_hip_error = 0;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int64_t kMaxGrid = std::numeric_limits<int32_t>::max();
 constexpr int kMinChunk = 256;    // keys per decode chunk chosen by the heuristic (one head per KV head)
-constexpr int kBlocksPerCu = 2;   // per-head decode workgroups per compute unit chosen by the heuristic
+constexpr int kBlocksPerCu = 1;   // per-head decode workgroups per compute unit chosen by the heuristic
 constexpr int kMinChunkGrouped = 128;   // grouped heads: at least one 32-key tile per wave
 
 bool shape_ok(int B, int Hq, int Hkv, int Lq, int Lk) {
@@ -148,10 +148,10 @@ int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D) {
     if (s < 1) s = 1;
     return (int)s;
   }
-  // The per-head kernel: about two workgroups per compute unit (measured
-  // with nontemporal K/V loads on four shapes, batch 1-32 and 2048-32768
-  // keys: within 1 % of the best split count on each, up to 7 % ahead of
-  // 8192 workgroups).
+  // The per-head kernel: about one workgroup per compute unit (measured at
+  // steady clock with nontemporal K/V loads on five shapes, batch 1-32,
+  // 2048-32768 keys, D 64 and 128: 2-4 % ahead of two per compute unit on
+  // four of them, 1 % behind on the ALiBi one).
   const int64_t groups = Hq / Hkv / decode_heads_per_block(Hq / Hkv);
   const int64_t units = (int64_t)B * Hkv * groups;
   const int64_t target = (int64_t)kBlocksPerCu * compute_units();

@@ -163,10 +163,11 @@ def test_workspace_check_uses_resolved_split_count(lib):
 
 
 def test_num_splits_heuristic(lib):
-    # One query head per KV head: about two workgroups per compute unit (256
+    # One query head per KV head: about one workgroup per compute unit (256
     # compute units without a device), chunks of >= 256 keys.
-    assert pa.attn_decode_num_splits(8, 32, 32, 8192, 128) == 2
-    assert pa.attn_decode_num_splits(1, 32, 32, 32768, 128) == 16
+    assert pa.attn_decode_num_splits(8, 32, 32, 8192, 128) == 1
+    assert pa.attn_decode_num_splits(1, 32, 32, 32768, 128) == 8
+    assert pa.attn_decode_num_splits(4, 32, 32, 16384, 64) == 2
     assert pa.attn_decode_num_splits(32, 32, 32, 2048, 128) == 1
     assert pa.attn_decode_num_splits(1, 1, 1, 1, 64) == 1
     assert pa.attn_decode_num_splits(1, 1, 1, 300, 64) == 2    # chunks of >= 256 keys
