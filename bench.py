@@ -5,8 +5,9 @@
 
 A step is one call of the library on one batch of a workload: attn_fwd(_mod)
 for a prefill workload (one kernel), attn_decode(_mod) for a decode workload
-(split kernel + combine kernel), norm_l2 / rmsnorm_rowmax for a row reduction
-(one kernel per row, or split kernel + combine kernel).  W untimed steps,
+(split kernel, and the combine kernel with more than one chunk), norm_l2 /
+rmsnorm_rowmax for a row reduction (one kernel per row, or split kernel +
+combine kernel).  W untimed steps,
 continued until at least WARMUP_MS of load has passed (so that the clock has
 risen), then K steps timed with HIP events recorded on the stream the kernels
 are launched on (the current torch stream, which the binding passes to the
@@ -230,6 +231,8 @@ def run_workload(name, steps, warmup, *, splits=0, errors=False):
             return lambda: pa.attn_decode(qs, ks, vs, o, scale=w.sm_scale, alibi_slopes=sl,
                                           softcap=w.softcap or None, num_splits=S, workspace=ws)
         kernels = pa.attn_decode_kernels(w.Hq, w.Hkv, w.D, q.dtype, sl is not None, w.softcap)
+        if S == 1:
+            kernels = kernels[:1]   # one chunk: the split kernel writes O, no combine runs
     else:
         S = None
 
@@ -542,7 +545,7 @@ def main():
         if WORKLOADS[name].decode:
             entry = {"workload": name, "value": r["GB/s"], "unit": "GB/s", "ms_per_step": r["ms_per_step"],
                      "num_splits": r["num_splits"],
-                     "roofline": hbm_roofline(r, "decode", name, peaks, "|Q|+|K|+|V|+|O|, split + combine kernels")}
+                     "roofline": hbm_roofline(r, "decode", name, peaks, "|Q|+|K|+|V|+|O|, split (+ combine) kernels")}
         else:
             entry = {"workload": name, "value": r["TFLOP/s"], "unit": "TFLOP/s", "ms_per_step": r["ms_per_step"],
                      "roofline": prefill_roofline(r, name, peaks, r["kernels"][0])}

@@ -160,6 +160,9 @@ int attn_decode_num_splits(int B, int Hq, int Hkv, int Lk, int D);
  *               after the call are the local partials described above.
  *
  * Two kernels run on `stream`: the local split kernel, then the combine.
+ * With one chunk (num_splits resolving to 1) the split kernel also writes O,
+ * exactly what the combine would compute from its single partial, and the
+ * combine does not run.
  * Errors: ATTN_ERR_NULL (Q, K, V, O or workspace NULL), ATTN_ERR_SHAPE,
  * ATTN_ERR_UNSUPPORTED, ATTN_ERR_WORKSPACE, ATTN_ERR_HIP.
  */
@@ -227,8 +230,8 @@ int attn_fwd_kernels(int D, attn_dtype dtype, int causal, int alibi, float softc
  * The kernels that attn_decode_mod (attn_decode: softcap = 0) launches, as
  * "split;combine" with the template arguments, e.g.
  * "decode_mfma_kernel<128,f16,0,0>;decode_combine_kernel<128,f16>" (local
- * and global nests of Fig. su-result).  Host only.  Errors as
- * attn_fwd_kernels.
+ * and global nests of Fig. su-result; with one chunk only the split kernel
+ * runs).  Host only.  Errors as attn_fwd_kernels.
  */
 int attn_decode_kernels(int Hq, int Hkv, int D, attn_dtype dtype, int alibi, float softcap, char* buf, size_t len);
 

@@ -228,6 +228,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
       p.ws_m[slot] = M == kNegInf ? kNegInf : M * kLn2;   // natural-log units
       p.ws_l[slot] = L;
     }
+    // One chunk: this partial is the whole row, and the output is what the
+    // combine kernel would compute from it (weight exp(0) = 1), which then
+    // does not run.
+    if (S == 1) reinterpret_cast<T*>(p.o)[(rowbase + g) * D + d] = (T)(L > 0.f ? acc / L : 0.f);
   }
 }
 
@@ -461,6 +465,10 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeParams p) {
       p.ws_m[slot] = M == kNegInf ? kNegInf : M * kLn2;   // natural-log units
       p.ws_l[slot] = L;
     }
+    // One chunk: this partial is the whole row, and the output is what the
+    // combine kernel would compute from it (weight exp(0) = 1), which then
+    // does not run.
+    if (S == 1) reinterpret_cast<T*>(p.o)[(rowbase + g) * D + d] = (T)(L > 0.f ? acc / L : 0.f);
   }
 }
 
@@ -537,7 +545,7 @@ hipError_t launch_split(const DecodeParams& p, hipStream_t stream) {
   else
     hipLaunchKernelGGL((decode_split_kernel<D, T, GH, false, false>), grid, block, 0, stream, p);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || p.splits == 1) return e;   // one chunk: the split kernel wrote O
   hipLaunchKernelGGL((decode_combine_kernel<D, T>), dim3(p.B * p.Hq), dim3(D), 0, stream, p);
   return hipGetLastError();
 }
@@ -555,7 +563,7 @@ hipError_t launch_mfma(const DecodeParams& p, hipStream_t stream) {
   else
     hipLaunchKernelGGL((decode_mfma_kernel<D, T, false, false>), grid, block, 0, stream, p);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || p.splits == 1) return e;   // one chunk: the split kernel wrote O
   hipLaunchKernelGGL((decode_combine_kernel<D, T>), dim3(p.B * p.Hq), dim3(D), 0, stream, p);
   return hipGetLastError();
 }

@@ -93,6 +93,22 @@ def test_decode_independent_of_split_count_and_equals_prefill_row():
         assert_close(o, outs[0], "decode(S) vs decode(1)")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (8, 2)], ids=["per-head", "grouped"])
+def test_one_chunk_output_is_the_combine_of_its_partial(Hq, Hkv):
+    """With one chunk the split kernel writes O itself (the combine does not
+    run); it must be what the combine computes from the single partial, whose
+    weight is exp(0) = 1: o_l / sum_l, rounded once to fp16."""
+    B, Lk, D = 2, 777, 128
+    print(f"one-chunk decode {B}x{Hq}/{Hkv} Lk {Lk}", flush=True)
+    q, k, v = random_tensors([(B, Hq, 1, D), (B, Hkv, Lk, D), (B, Hkv, Lk, D)], "f16", seed=37)
+    o, ws, S = run_decode(q, k, v, scale=D ** -0.5, num_splits=1)
+    ol, _, sl = (t.cpu().numpy() for t in pa.decode_partials(ws, B, Hq, D, 1))
+    expect = (ol[:, :, 0] / sl[:, :, 0, None]).astype(np.float16)
+    got = o.cpu().numpy().reshape(B, Hq, D)
+    assert np.array_equal(got.view(np.uint16), expect.view(np.uint16))
+    assert_close(host32(o), oracle_fwd(q, k, v, scale=D ** -0.5, causal=True), "one-chunk decode vs oracle")
+
+
 def test_decode_is_deterministic():
     q, k, v = random_tensors([(4, 8, 1, 128), (4, 2, 5000, 128), (4, 2, 5000, 128)], "bf16", seed=32)
     a = run_decode(q, k, v, scale=0.1, num_splits=13)[0]
