@@ -10,10 +10,11 @@
 // the workgroup's registers, writes y from them without reading X again.
 //
 // Cache policy: X is read once by the L2 norm and by the one-pass RMSNorm,
-// and last by RMSNorm's second kernel, so those loads (and the stores of y)
-// are nontemporal; RMSNorm's first pass reads X with ordinary loads so that
-// the second pass finds what the caches (L2 and the memory-side cache) still
-// hold of it.
+// and last by RMSNorm's second kernel, so those loads are nontemporal, and
+// so are the second kernel's stores of y; RMSNorm's first pass reads X with
+// ordinary loads so that the second pass finds what the caches (L2 and the
+// memory-side cache) still hold of it.  (The one-pass kernel's stores of y
+// are ordinary: 1.5 % faster there.)
 
 #include <type_traits>
 
@@ -305,16 +306,19 @@ __global__ __launch_bounds__(kRowThreads) void rms_row_kernel(NormParams p) {
   const int nv = p.M / VN;
   const u32x4* row = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.x) + (size_t)n * p.M);
   u32x4* yrow = reinterpret_cast<u32x4*>(reinterpret_cast<T*>(p.y) + (size_t)n * p.M);
+  // Rows of exactly kRowThreads x kRowVecs vectors take no per-vector
+  // branches (measured 0.8 % faster).
+  const bool full = nv == kRowThreads * kRowVecs;
   u32x4 w[kRowVecs];
 #pragma unroll
   for (int u = 0; u < kRowVecs; ++u) {
     const int v = threadIdx.x + u * kRowThreads;
-    w[u] = v < nv ? load16<true>(row + v) : u32x4{0u, 0u, 0u, 0u};
+    w[u] = (full || v < nv) ? load16<true>(row + v) : u32x4{0u, 0u, 0u, 0u};
   }
   RmsState st;
 #pragma unroll
   for (int u = 0; u < kRowVecs; ++u) {
-    if (threadIdx.x + u * kRowThreads < nv) {
+    if (full || threadIdx.x + u * kRowThreads < nv) {
       float f[VN];
       Vec<T>::load(w[u], f);
       st.template fold<VN>(f, p.invM, p.eps);
@@ -341,7 +345,7 @@ __global__ __launch_bounds__(kRowThreads) void rms_row_kernel(NormParams p) {
       Vec<T>::load(w[u], f);
 #pragma unroll
       for (int k = 0; k < VN; ++k) f[k] *= q;
-      __builtin_nontemporal_store(Vec<T>::store(f), yrow + v);
+      yrow[v] = Vec<T>::store(f);
     }
   }
 }
