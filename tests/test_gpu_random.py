@@ -17,7 +17,7 @@ from paper_2510_08726_amd.workloads import NORM_DTYPES, alibi_slopes, random_ten
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 24
+N_CASES = 48
 
 
 def assert_close_attributed(got, ref, dt, what):
