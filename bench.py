@@ -479,7 +479,7 @@ def main():
     args = parse()
     WARMUP_MS = args.warmup_ms
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on exactly one GPU (no multi-GPU path); "
+        print("bench.py: this library runs on exactly one GPU (no multi-GPU path); "
               "use --gpus 1", file=sys.stderr)
         sys.exit(2)
     import torch
