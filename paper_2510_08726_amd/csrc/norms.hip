@@ -30,6 +30,8 @@ constexpr int kL2RowThreads = 256;   // the L2 norm with one chunk per row
 constexpr int kL2RowUnroll = 16;     // its 16-byte loads in flight per lane
 constexpr int kRowThreads = 1024;    // the one-pass RMSNorm: one row per workgroup
 constexpr int kRowVecs = (int)(kNormRowBytes / (kRowThreads * 16));   // 16-byte vectors per lane
+constexpr int kRowBatch = 2;         // of which loaded (and folded) at a time
+static_assert(kRowVecs % kRowBatch == 0, "whole batches");
 constexpr int kNormUnroll = 8;    // 16-byte loads in flight per lane, first pass
 constexpr int kApplyUnroll = 4;   // the same in RMSNorm's second pass
 
@@ -309,23 +311,33 @@ __global__ __launch_bounds__(kRowThreads) void rms_row_kernel(NormParams p) {
   // Rows of exactly kRowThreads x kRowVecs vectors take no per-vector
   // branches (measured 0.8 % faster).
   const bool full = nv == kRowThreads * kRowVecs;
+  // The row is read in batches of kRowBatch vectors a lane, each folded
+  // before the next is issued (the empty asm with a memory clobber keeps the
+  // next batch's loads after the fold): 2 vectors a lane, 32 KiB of loads in
+  // flight per workgroup, measured 5.33 TB/s on 256 x 2^17 bf16 rows against
+  // 4.78 with the whole row's 16 vectors in flight at once (4 a batch: 5.13;
+  // 1: 5.03).
   u32x4 w[kRowVecs];
-#pragma unroll
-  for (int u = 0; u < kRowVecs; ++u) {
-    const int v = threadIdx.x + u * kRowThreads;
-    w[u] = (full || v < nv) ? load16<true>(row + v) : u32x4{0u, 0u, 0u, 0u};
-  }
   RmsState st;
 #pragma unroll
-  for (int u = 0; u < kRowVecs; ++u) {
-    if (full || threadIdx.x + u * kRowThreads < nv) {
-      float f[VN];
-      Vec<T>::load(w[u], f);
-      st.template fold<VN>(f, p.invM, p.eps);
+  for (int b0 = 0; b0 < kRowVecs; b0 += kRowBatch) {
+#pragma unroll
+    for (int u = b0; u < b0 + kRowBatch; ++u) {
+      const int v = threadIdx.x + u * kRowThreads;
+      w[u] = (full || v < nv) ? load16<true>(row + v) : u32x4{0u, 0u, 0u, 0u};
     }
-    // Keep the loaded words, not their conversions, live until the stores
-    // (half the registers for fp16 and bf16).
-    asm volatile("" : "+v"(w[u]));
+#pragma unroll
+    for (int u = b0; u < b0 + kRowBatch; ++u) {
+      if (full || threadIdx.x + u * kRowThreads < nv) {
+        float f[VN];
+        Vec<T>::load(w[u], f);
+        st.template fold<VN>(f, p.invM, p.eps);
+      }
+      // Keep the loaded words, not their conversions, live until the stores
+      // (half the registers for fp16 and bf16).
+      asm volatile("" : "+v"(w[u]));
+    }
+    asm volatile("" ::: "memory");
   }
   block_merge<kRowThreads>(st, p.eps);
   __shared__ float s_q;
